@@ -1,0 +1,199 @@
+"""Benchmark: one verification round per step on one MI355X.
+
+A step is the whole hot path on one batch: kv_gather of the arriving
+requests' blocks, verify_attention over every layer, spec_accept.  Inputs
+(synthetic, seeded) are resident in HBM before timing starts.  Prints ONE JSON
+line; see DESIGN.md for the byte accounting behind "roofline".
+
+    python bench.py [--steps K] [--warmup W] [--workload verify_8b] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak, GB/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="verify_8b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def describe(cfg):
+    return {"workload": cfg.name, "bs": cfg.bs, "layers": cfg.num_layers,
+            "q_heads": cfg.num_q_heads, "kv_heads": cfg.num_kv_heads, "head_dim": cfg.head_dim,
+            "context": [cfg.ctx_lo, cfg.ctx_hi], "draft_len": [cfg.k_lo, cfg.k_hi],
+            "arriving": cfg.n_arriving, "vocab": cfg.vocab, "block_size": cfg.block_size,
+            "seed": cfg.seed}
+
+
+def algorithmic_bytes(cfg, meta, acc_len=None):
+    """Bytes each step must move at minimum (read + write), per kernel."""
+    hkv, d, hq = cfg.num_kv_heads, cfg.head_dim, cfg.num_q_heads
+    block_bytes = hkv * 16 * d * 2
+    gather = 2 * meta.n_pairs * 2 * block_bytes * cfg.num_layers
+    kv_tokens = int(meta.seq_lens.astype(np.int64).sum())
+    attn = cfg.num_layers * (kv_tokens * 2 * hkv * d * 2 + 2 * meta.total_q * hq * d * 2)
+    accept = 0
+    if cfg.vocab and acc_len is not None:
+        rows = np.where(acc_len < meta.depth, 2, 1).sum()
+        accept = int(rows) * cfg.vocab * 4 + meta.total_q * 4 * 3
+    return gather, attn, accept
+
+
+def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
+    """The CPU oracle, untuned, on a bounded sample of the same round."""
+    import oracle
+    from workload.synth import logical_kv
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    rng = np.random.default_rng(0)
+    order = rng.permutation(cfg.bs)
+    p = acc_in.p_target if acc_in is not None else None
+    done, t_total = 0, 0.0
+    u16 = lambda t: t.view(__import__("torch").int16).cpu().numpy()
+    for r in order:
+        # host copies of this request's inputs (not timed)
+        nb = meta.nblk(r)
+        k, v = logical_kv(meta, layer, r)
+        k64, v64 = k.double().cpu().numpy(), v.double().cpu().numpy()
+        a, b = int(meta.q_indptr[r]), int(meta.q_indptr[r + 1])
+        q64 = layer.q[a:b].double().cpu().numpy()
+        if meta.arriving[r]:
+            ids = meta.stage_table[r, :nb]
+            sk, sv = u16(layer.k_stage[ids])[None], u16(layer.v_stage[ids])[None]
+            dk = np.zeros_like(sk)
+            dv = np.zeros_like(sv)
+        if acc_in is not None:
+            kk = b - a - 1
+            pr = acc_in.p_target[a:b].cpu().numpy()
+            qr = acc_in.q_draft[a - r:a - r + kk].cpu().numpy()
+            xr = acc_in.draft_tokens[a - r:a - r + kk].cpu().numpy()
+            ur = acc_in.uniforms[a:b].cpu().numpy()
+        t0 = time.perf_counter()
+        if meta.arriving[r]:
+            oracle.gather.kv_gather(sk, sv, dk, dv, np.arange(nb), np.arange(nb))
+        oracle.attention.verify_attention_request(q64, k64, v64, 1.0 / np.sqrt(cfg.head_dim))
+        if acc_in is not None:
+            oracle.accept.accept_request(pr, qr, xr, ur)
+        t_total += time.perf_counter() - t0
+        done += 1
+        if t_total >= budget_s and done >= 2:
+            break
+    layers = cfg.num_layers
+    per_req = t_total / done * layers if layers > 1 else t_total / done
+    return {"value": round(1.0 / per_req, 3), "unit": "requests/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} of {cfg.bs} requests of the {cfg.name} round (gather of their "
+                      f"blocks if arriving, attention over all heads/queries, acceptance), "
+                      f"{t_total:.1f} s of fp64 numpy"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; use --gpus 1"}))
+        sys.exit(2)
+    import torch
+    import paper_2609_29364_amd as nsd
+    from workload import CONFIGS, make_meta, make_layer, make_accept
+
+    if not os.path.exists(nsd.LIB_PATH):
+        from paper_2609_29364_amd.build import build
+        build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.workload]
+    if cfg.num_layers != 1:
+        raise SystemExit("bench times single-layer workloads; the 36-layer round is a test case")
+    meta = make_meta(cfg)
+    layer = make_layer(cfg, meta, 0, dev)
+    acc_in = make_accept(cfg, meta, dev)
+    i32 = lambda a: torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32, device=dev)
+    src, dst = i32(meta.src_ids), i32(meta.dst_ids)
+    bt, sl, qi = i32(meta.block_table), i32(meta.seq_lens), i32(meta.q_indptr)
+    kp, vp = layer.k_pool, layer.v_pool
+    ks, vs = layer.k_stage, layer.v_stage
+    out = torch.empty_like(layer.q)
+    ws_n = nsd.verify_attention_workspace_size(cfg.bs, cfg.num_q_heads, cfg.num_kv_heads,
+                                               cfg.head_dim, meta.max_q, meta.max_seq_len)
+    ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device=dev)
+    acc_len = torch.empty(cfg.bs, dtype=torch.int32, device=dev)
+    toks = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        nsd.kv_gather(ks, vs, kp, vp, src, dst)
+        if ev: ev[1].record(stream)
+        nsd.verify_attention(layer.q, kp, vp, bt, sl, qi, meta.max_q, meta.max_seq_len,
+                             out=out, workspace=ws)
+        if ev: ev[2].record(stream)
+        if acc_in is not None:
+            nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
+                            acc_in.uniforms, qi, cfg.k_hi, accepted_len=acc_len, out_tokens=toks)
+        if ev: ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+    parts = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                      for e in evs])
+    g_ms, a_ms, c_ms = parts.mean(0)
+    acc_host = acc_len.cpu().numpy() if acc_in is not None else None
+    gb, ab, cb = algorithmic_bytes(cfg, meta, acc_host)
+    achieved = ab / (a_ms * 1e-3) / 1e9
+    result = {
+        "metric": "verify-round requests/s (8B-shaped layer, bs=256, K=4); achieved HBM TB/s",
+        "value": round(cfg.bs / (ms_step * 1e-3), 1),
+        "unit": "requests/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": describe(cfg),
+        "breakdown_ms": {"kv_gather": round(g_ms, 5), "verify_attention": round(a_ms, 5),
+                         "spec_accept": round(c_ms, 5)},
+        "round_hbm_tbs": round((gb + ab + cb) / (ms_step * 1e-3) / 1e12, 3),
+        "gather_attention_tbs": round((gb + ab) / ((g_ms + a_ms) * 1e-3) / 1e12, 3),
+        "roofline": {"bound": "hbm", "kernel": "verify_attention", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "alg_bytes_per_launch": ab},
+        "wall_s_timed": round(t_wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cfg, meta, layer, acc_in, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

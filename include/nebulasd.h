@@ -1,0 +1,190 @@
+/*
+ * nebulasd.h -- C ABI of the verification-round library (libnebulasd.so).
+ *
+ * One speculative verification round on a reconstructed batch (NebulaSD,
+ * Algorithm 1: Prepare then Run) is three calls on one HIP stream:
+ *
+ *   nsd_kv_gather         KV-state preparation of arriving requests
+ *   nsd_verify_attention  grouped-query attention of the anchor + K proposal
+ *                         queries of every request over the paged KV cache
+ *   nsd_spec_accept       acceptance of proposals and residual resampling
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers named as device pointers must address memory the GPU of
+ *   `stream` can read/write; all work is enqueued on `stream` (a hipStream_t,
+ *   NULL = the null stream) and the call returns without waiting.  The caller
+ *   owns every buffer, including workspaces, and keeps it alive until the
+ *   stream has passed the call.  The library allocates nothing and keeps no
+ *   state besides a thread-local error message.
+ * - Arguments are validated on the host before anything is enqueued; a bad
+ *   scalar or NULL pointer returns an error status and enqueues nothing.
+ *   Device-resident contents (block ids, lengths, offsets, tokens) are not
+ *   visible to the host: contents outside the documented ranges give
+ *   unspecified results, but every kernel clamps them so that it never reads
+ *   or writes outside the buffers whose sizes the scalars describe.
+ * - Calls never abort and never print.  Calls on different streams with
+ *   disjoint outputs may run concurrently.
+ * - bf16 is bfloat16 (1 sign, 8 exponent, 7 mantissa bits) stored in 2 bytes.
+ *
+ * Paged KV layout (Section 3: paged KV blocks; Appendix E.1: separate K and V
+ * planes).  A block holds BLOCK_SIZE = 16 consecutive token slots of one
+ * request for every KV head.  Per layer:
+ *   K plane: bf16 [num_blocks][num_kv_heads][head_dim/8][16][8]
+ *            (16-byte runs of 8 dimensions; the 16 slots of one run index are
+ *            adjacent)
+ *   V plane: bf16 [num_blocks][num_kv_heads][head_dim][16]
+ *            (the 16 slots of one dimension are adjacent)
+ * A multi-layer pool stacks layers outermost: [num_layers][num_blocks][...].
+ * Token t of a request lives in slot t % 16 of block block_table[r][t / 16].
+ */
+#ifndef NEBULASD_H
+#define NEBULASD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t nsd_status;
+
+#define NSD_OK              0
+#define NSD_ERR_NULL        1  /* a required pointer is NULL */
+#define NSD_ERR_SHAPE       2  /* a size/count argument is out of range */
+#define NSD_ERR_UNSUPPORTED 3  /* valid in principle, not implemented (e.g. head_dim) */
+#define NSD_ERR_WORKSPACE   4  /* workspace pointer NULL or smaller than required */
+#define NSD_ERR_HIP         5  /* the HIP runtime reported an error; see nsd_last_error */
+
+#define NSD_BLOCK_SIZE 16
+
+/* Library version, (major << 16) | minor. */
+int32_t nsd_version(void);
+
+/* Message describing the last non-OK status returned on the calling thread.
+   Valid until the next library call on that thread.  Never NULL. */
+const char* nsd_last_error(void);
+
+/*
+ * KV-state preparation: copy whole KV blocks of arriving requests from a
+ * staging pool into the worker's paged pool.
+ *
+ * Passage: Algorithm 1 (Prepare(B, w) makes the batch's KV state resident on
+ * worker w before Run); Appendix E.1 (each request's state sits in a stable
+ * extent of blocks, Eq. E.1, addressed by numeric offsets); Appendix E.4
+ * (copy plans travel as compact descriptors).
+ *
+ * For every pair i in [0, n_pairs) and every layer l in [layer0, layer0+n_layers):
+ *     dst_k[l][dst_ids[i]] <- src_k[l][src_ids[i]]
+ *     dst_v[l][dst_ids[i]] <- src_v[l][src_ids[i]]
+ * copying the whole block (all KV heads, all 16 slots).  Blocks not named by
+ * dst_ids are not written.
+ *
+ * src_k, src_v : device, bf16 [num_layers][src_num_blocks][block], layout above.
+ * dst_k, dst_v : device, bf16 [num_layers][dst_num_blocks][block].
+ * src_ids, dst_ids : device, int32 [n_pairs].  Ids must lie in [0, src_num_blocks)
+ *                / [0, dst_num_blocks) and dst_ids must be distinct; a pair with
+ *                an id out of range is skipped.
+ * num_layers : layers in both pools; 0 <= layer0, layer0 + n_layers <= num_layers.
+ * num_kv_heads >= 1, block_size == 16, head_dim in {64, 128}.
+ * n_pairs == 0 or n_layers == 0 is a no-op returning NSD_OK.
+ * Source and destination must not overlap.
+ */
+nsd_status nsd_kv_gather(const void* src_k, const void* src_v, int64_t src_num_blocks,
+                         void* dst_k, void* dst_v, int64_t dst_num_blocks,
+                         const int32_t* src_ids, const int32_t* dst_ids, int64_t n_pairs,
+                         int32_t num_layers, int32_t layer0, int32_t n_layers,
+                         int32_t num_kv_heads, int32_t block_size, int32_t head_dim,
+                         void* stream);
+
+/*
+ * Bytes of workspace nsd_verify_attention needs for these sizes (0 if the
+ * sizes are invalid).  Depends only on its arguments.
+ */
+size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
+                                           int32_t num_kv_heads, int32_t head_dim,
+                                           int32_t max_q_per_seq, int32_t max_seq_len);
+
+/*
+ * Verification attention for one layer.
+ *
+ * Passage: Section 1 (the target model verifies the draft's proposals in one
+ * forward pass); Appendix G.2 and H (a round scores the anchor token plus d
+ * proposal tokens per request); Section 3 (the KV cache is paged and
+ * append-dominant: it already holds the window's states).
+ *
+ * Request r has n_q = q_indptr[r+1] - q_indptr[r] query tokens (anchor plus
+ * K_r proposals) and L_r = seq_lens[r] cached tokens including those n_q.
+ * Query j sits at position L_r - n_q + j and attends to tokens 0 .. L_r-n_q+j
+ * of its request.  Query head h reads KV head h / (num_q_heads/num_kv_heads).
+ *     out[q_indptr[r]+j][h] = softmax_t(scale * <q, k_t>) . v_t
+ * computed from bf16 inputs with fp32 accumulation; out is rounded to bf16.
+ * A query row with no visible token (only if n_q > L_r) is written as 0.
+ *
+ * q        : device, bf16 [total_q][num_q_heads][head_dim], total_q = q_indptr[bs].
+ * k_cache, v_cache : device, this layer's planes, [num_blocks][...] (layout above).
+ * block_table : device, int32 [bs][max_blocks_per_seq]; entries past
+ *               ceil(L_r/16) are not read.  Ids outside [0, num_blocks) make
+ *               their block's tokens invisible.
+ * seq_lens : device, int32 [bs], 1 <= L_r <= max_seq_len, L_r <= 16*max_blocks_per_seq.
+ * q_indptr : device, int32 [bs+1], non-decreasing, q_indptr[0] = 0,
+ *            1 <= n_q <= min(max_q_per_seq, L_r).
+ * num_q_heads % num_kv_heads == 0; (num_q_heads/num_kv_heads) * max_q_per_seq <= 64.
+ * head_dim in {64, 128}; block_size == 16.
+ * scale : the softmax scale (usually 1/sqrt(head_dim)), finite.
+ * out : device, bf16 [total_q][num_q_heads][head_dim]; may not alias q or the caches.
+ * workspace : device, at least nsd_verify_attention_workspace_size(...) bytes
+ *             (may be NULL when that size is 0).  Its contents on entry do not
+ *             matter; it is scratch for split partial results.
+ * bs == 0 is a no-op returning NSD_OK.
+ */
+nsd_status nsd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
+                                int64_t num_blocks, const int32_t* block_table,
+                                int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                const int32_t* q_indptr, int32_t bs, int32_t num_q_heads,
+                                int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                                int32_t max_q_per_seq, int32_t max_seq_len, float scale,
+                                void* out, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
+/*
+ * Speculative acceptance with residual resampling.
+ *
+ * Passage: Sections 1 and 2 (speculative decoding as in Leviathan et al. 2023
+ * and Chen et al. 2023, which the paper cites for the verification rule).
+ *
+ * Request r has K_r = q_indptr[r+1] - q_indptr[r] - 1 proposals.  Its target
+ * rows are p_target[q_indptr[r] + i] (i = 0..K_r), its draft rows and
+ * proposal tokens q_draft[q_indptr[r] - r + i] and draft_tokens[q_indptr[r] - r + i]
+ * (i = 0..K_r-1), its uniforms uniforms[q_indptr[r] + i] (i = 0..K_r: K_r
+ * acceptance uniforms then one sampling uniform).
+ *   1. Proposal i is accepted iff u_i * q_i(x_i) <= p_i(x_i), evaluated exactly
+ *      (fp64 product of fp32 values); n = first rejected i, or K_r.  A proposal
+ *      token outside [0, vocab) is rejected.
+ *   2. Weights w = max(0, p_n - q_n) if n < K_r (p_n if that has no mass),
+ *      else w = p_{K_r} (the bonus row); accumulated in fp64.
+ *   3. y = min{t : C(t) > u_{K_r} * C(vocab-1)}, C the inclusive prefix sum of
+ *      w in token order (last token of positive weight if rounding leaves none);
+ *      a token of zero weight is never emitted.
+ * Outputs: accepted_len[r] = n; out_tokens[q_indptr[r] + i] = x_i for i < n,
+ * y at i = n, -1 for n < i <= K_r.
+ *
+ * p_target : device, fp32 [total_q][vocab];  q_draft : device, fp32 [total_q-bs][vocab]
+ * draft_tokens : device, int32 [total_q-bs];  uniforms : device, fp32 [total_q], in [0,1)
+ * q_indptr : device, int32 [bs+1], q_indptr[0] = 0, 0 <= K_r <= max_k.
+ * vocab : 4 <= vocab <= 2^19, vocab % 4 == 0; 0 <= max_k <= 63.
+ * accepted_len : device, int32 [bs];  out_tokens : device, int32 [total_q].
+ * Row bases must be 16-byte aligned (true for cudaMalloc'd/torch tensors).
+ * q_draft and draft_tokens may be NULL when max_k == 0.  bs == 0 is a no-op.
+ */
+nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
+                           const int32_t* draft_tokens, const float* uniforms,
+                           const int32_t* q_indptr, int32_t bs, int32_t vocab, int32_t max_k,
+                           int32_t* accepted_len, int32_t* out_tokens, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NEBULASD_H */

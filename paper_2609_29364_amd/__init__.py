@@ -1,0 +1,189 @@
+"""Python binding of libnebulasd, the MI355X verification-round library.
+
+Thin argument marshalling over the C ABI declared in ``include/nebulasd.h``:
+torch tensors are checked (dtype, device, contiguity, shapes) and passed as
+raw device pointers together with torch's current HIP stream.  Every step of
+the round runs in the library's HIP kernels; there is no fallback, and a
+missing library raises at the first call.
+"""
+import ctypes
+import math
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnebulasd.so")
+BLOCK_SIZE = 16
+
+STATUS_NAMES = {0: "NSD_OK", 1: "NSD_ERR_NULL", 2: "NSD_ERR_SHAPE", 3: "NSD_ERR_UNSUPPORTED",
+                4: "NSD_ERR_WORKSPACE", 5: "NSD_ERR_HIP"}
+
+
+class NsdError(RuntimeError):
+    def __init__(self, fn, status, message):
+        super().__init__(f"{fn}: {STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+_P, _I32, _I64, _F32, _SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                             ctypes.c_size_t)
+_SIGS = {
+    "nsd_version": (_I32, []),
+    "nsd_last_error": (ctypes.c_char_p, []),
+    "nsd_kv_gather": (_I32, [_P, _P, _I64, _P, _P, _I64, _P, _P, _I64, _I32, _I32, _I32, _I32,
+                             _I32, _I32, _P]),
+    "nsd_verify_attention_workspace_size": (_SZ, [_I32, _I32, _I32, _I32, _I32, _I32]),
+    "nsd_verify_attention": (_I32, [_P, _P, _P, _I64, _P, _I32, _P, _P, _I32, _I32, _I32, _I32,
+                                    _I32, _I32, _I32, _F32, _P, _P, _SZ, _P]),
+    "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
+}
+
+
+def lib():
+    """The loaded library (torch's HIP runtime is loaded first and shared)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -c \"import "
+                               f"__graft_entry__ as g; g.build()\"` at the repository root")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(l, name)
+            f.restype, f.argtypes = res, args
+        _lib = l
+    return _lib
+
+
+def _check(fn, status):
+    if status != 0:
+        raise NsdError(fn, status, lib().nsd_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t, dtype, name):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream(t):
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def version():
+    v = lib().nsd_version()
+    return (v >> 16, v & 0xFFFF)
+
+
+def kv_gather(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, layer0=0, n_layers=None):
+    """Copy whole KV blocks src -> dst for every pair and layer (in place on dst).
+
+    Planes: K [layers][blocks][Hkv][D/8][16][8], V [layers][blocks][Hkv][D][16] bf16
+    (a 5-d tensor is taken as a single layer).  src_ids/dst_ids: int32 [n_pairs].
+    """
+    planes = [src_k, src_v, dst_k, dst_v]
+    if src_k.dim() == 5:
+        planes = [t.unsqueeze(0) for t in planes]
+    sk, sv, dk, dv = planes
+    for t, n in zip(planes, ("src_k", "src_v", "dst_k", "dst_v")):
+        _dev(t, torch.bfloat16, n)
+    _dev(src_ids, torch.int32, "src_ids")
+    _dev(dst_ids, torch.int32, "dst_ids")
+    num_layers, _, hkv, dv8, bsz, vec = sk.shape
+    d = dv8 * vec
+    if (sv.shape != (num_layers, sk.shape[1], hkv, d, bsz) or dk.shape[0] != num_layers
+            or dk.shape[2:] != sk.shape[2:] or dv.shape != (num_layers, dk.shape[1], hkv, d, bsz)):
+        raise ValueError("inconsistent pool shapes")
+    if src_ids.numel() != dst_ids.numel():
+        raise ValueError("src_ids and dst_ids differ in length")
+    if n_layers is None:
+        n_layers = num_layers - layer0
+    _check("kv_gather", lib().nsd_kv_gather(
+        _ptr(sk), _ptr(sv), sk.shape[1], _ptr(dk), _ptr(dv), dk.shape[1], _ptr(src_ids),
+        _ptr(dst_ids), src_ids.numel(), num_layers, layer0, n_layers, hkv, bsz, d, _stream(sk)))
+    return dst_k, dst_v
+
+
+def verify_attention_workspace_size(bs, num_q_heads, num_kv_heads, head_dim, max_q_per_seq,
+                                    max_seq_len):
+    return int(lib().nsd_verify_attention_workspace_size(bs, num_q_heads, num_kv_heads, head_dim,
+                                                         max_q_per_seq, max_seq_len))
+
+
+def verify_attention(q, k_cache, v_cache, block_table, seq_lens, q_indptr, max_q_per_seq,
+                     max_seq_len, scale=None, out=None, workspace=None):
+    """One layer of verification attention; returns out [total_q][Hq][D] bf16.
+
+    k_cache [blocks][Hkv][D/8][16][8], v_cache [blocks][Hkv][D][16] bf16;
+    block_table int32 [bs][max_blocks]; seq_lens int32 [bs]; q_indptr int32 [bs+1].
+    max_q_per_seq / max_seq_len are host-side bounds of n_q and L_r.
+    """
+    _dev(q, torch.bfloat16, "q")
+    _dev(k_cache, torch.bfloat16, "k_cache")
+    _dev(v_cache, torch.bfloat16, "v_cache")
+    for t, n in ((block_table, "block_table"), (seq_lens, "seq_lens"), (q_indptr, "q_indptr")):
+        _dev(t, torch.int32, n)
+    total_q, hq, d = q.shape
+    nb, hkv, dv8, bsz, vec = k_cache.shape
+    if dv8 * vec != d or v_cache.shape != (nb, hkv, d, bsz):
+        raise ValueError("cache shapes do not match q")
+    bs = seq_lens.numel()
+    if block_table.dim() != 2 or block_table.shape[0] != bs or q_indptr.numel() != bs + 1:
+        raise ValueError("block_table / q_indptr do not match seq_lens")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _dev(out, torch.bfloat16, "out")
+        if out.shape != q.shape:
+            raise ValueError("out must have q's shape")
+    need = verify_attention_workspace_size(bs, hq, hkv, d, max_q_per_seq, max_seq_len)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("verify_attention", lib().nsd_verify_attention(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), nb, _ptr(block_table), block_table.shape[1],
+        _ptr(seq_lens), _ptr(q_indptr), bs, hq, hkv, d, bsz, max_q_per_seq, max_seq_len,
+        float(scale), _ptr(out), _ptr(workspace), ws_bytes, _stream(q)))
+    return out
+
+
+def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, accepted_len=None,
+                out_tokens=None):
+    """Acceptance + residual resampling; returns (accepted_len [bs], out_tokens [total_q]) int32."""
+    _dev(p_target, torch.float32, "p_target")
+    _dev(uniforms, torch.float32, "uniforms")
+    _dev(q_indptr, torch.int32, "q_indptr")
+    if max_k > 0:
+        _dev(q_draft, torch.float32, "q_draft")
+        _dev(draft_tokens, torch.int32, "draft_tokens")
+    total_q, vocab = p_target.shape
+    bs = q_indptr.numel() - 1
+    if uniforms.numel() != total_q:
+        raise ValueError("uniforms must have one entry per target row")
+    if max_k > 0 and (q_draft.shape != (total_q - bs, vocab) or draft_tokens.numel() != total_q - bs):
+        raise ValueError("q_draft / draft_tokens must have total_q - bs rows")
+    if accepted_len is None:
+        accepted_len = torch.empty(bs, dtype=torch.int32, device=p_target.device)
+    if out_tokens is None:
+        out_tokens = torch.empty(total_q, dtype=torch.int32, device=p_target.device)
+    _dev(accepted_len, torch.int32, "accepted_len")
+    _dev(out_tokens, torch.int32, "out_tokens")
+    _check("spec_accept", lib().nsd_spec_accept(
+        _ptr(p_target), _ptr(q_draft) if max_k > 0 else None,
+        _ptr(draft_tokens) if max_k > 0 else None, _ptr(uniforms), _ptr(q_indptr), bs, vocab,
+        max_k, _ptr(accepted_len), _ptr(out_tokens), _stream(p_target)))
+    return accepted_len, out_tokens
+
+
+__all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
+           "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

@@ -1,0 +1,300 @@
+"""GPU parity on small rounds: every step against the oracle, element by element,
+plus edge cases (ragged depths, L mod 16 in {0, 1, 15}, L = n_q, every GQA
+group size, both head dims, forced context splits)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_29364_amd as nsd
+from paper_2609_29364_amd.round import verify_round
+from workload import CONFIGS, custom_config, make_meta, make_layer, make_accept
+from parity import i32, u16, check_attention, check_accept
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_round(cfg, meta, dev, layers=None, accept=True, split_tokens=None):
+    layers = layers or [make_layer(cfg, meta, l, "cpu") for l in range(cfg.num_layers)]
+    stack = lambda name: torch.stack([getattr(l, name) for l in layers]).to(dev).contiguous()
+    kp, vp, ks, vs, q = (stack(n) for n in ("k_pool", "v_pool", "k_stage", "v_stage", "q"))
+    acc_in = make_accept(cfg, meta, "cpu") if (accept and cfg.vocab) else None
+    acc_dev = None
+    if acc_in is not None:
+        acc_dev = (acc_in.p_target.to(dev), acc_in.q_draft.to(dev), acc_in.draft_tokens.to(dev),
+                   acc_in.uniforms.to(dev), int(meta.depth.max()))
+    old = os.environ.get("NSD_SPLIT_TOKENS")
+    if split_tokens:
+        os.environ["NSD_SPLIT_TOKENS"] = str(split_tokens)
+    try:
+        outs, acc, tok = verify_round(kp, vp, ks, vs, i32(meta.src_ids, dev), i32(meta.dst_ids, dev),
+                                      q, i32(meta.block_table, dev), i32(meta.seq_lens, dev),
+                                      i32(meta.q_indptr, dev), meta.max_q, meta.max_seq_len,
+                                      accept=acc_dev)
+        torch.cuda.synchronize()
+    finally:
+        if split_tokens:
+            if old is None:
+                del os.environ["NSD_SPLIT_TOKENS"]
+            else:
+                os.environ["NSD_SPLIT_TOKENS"] = old
+    return layers, kp, vp, outs, acc_in, acc, tok
+
+
+def _check_all(cfg, meta, dev, **kw):
+    layers, kp, vp, outs, acc_in, acc, tok = _run_round(cfg, meta, dev, **kw)
+    ref_k, ref_v = oracle.gather.kv_gather(
+        np.stack([u16(l.k_stage) for l in layers]), np.stack([u16(l.v_stage) for l in layers]),
+        np.stack([u16(l.k_pool) for l in layers]), np.stack([u16(l.v_pool) for l in layers]),
+        meta.src_ids, meta.dst_ids)
+    assert np.array_equal(u16(kp), ref_k) and np.array_equal(u16(vp), ref_v)
+    for l, lay in enumerate(layers):
+        check_attention(meta, lay, outs[l], range(cfg.bs))
+    if acc_in is not None:
+        check_accept(acc_in.p_target.numpy(), acc_in.q_draft.numpy(),
+                     acc_in.draft_tokens.numpy(), acc_in.uniforms.numpy(), meta.q_indptr,
+                     acc.cpu().numpy(), tok.cpu().numpy())
+    return outs
+
+
+def test_tiny_round(device):
+    cfg = CONFIGS["tiny"]
+    _check_all(cfg, make_meta(cfg), device)
+
+
+def test_tiny_round_shuffled_staging(device):
+    cfg = custom_config(staging_order="shuffled", seed=10)
+    _check_all(cfg, make_meta(cfg), device)
+
+
+CASES = [
+    # (Hq, Hkv, D, seq_lens, depths)
+    (4, 4, 64, [16, 17, 31], [4, 0, 2]),
+    (4, 2, 128, [1, 33, 47, 64], [0, 8, 3, 1]),
+    (32, 8, 128, [5, 100, 513, 1024, 1500], [4, 4, 4, 4, 4]),
+    (8, 1, 64, [8, 64, 65, 300], [7, 6, 5, 4]),
+    (16, 8, 128, [1, 2, 15, 16, 17, 31, 32, 33], [0, 0, 0, 0, 0, 0, 0, 0]),
+    (32, 8, 64, [9, 47, 48, 49, 95, 96], [8, 8, 8, 8, 8, 8]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("split", [None, 32, 96])
+def test_attention_edge_cases(device, case, split):
+    hq, hkv, d, lens, depth = CASES[case]
+    bs = len(lens)
+    cfg = custom_config(seed=100 + case, bs=bs, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                        vocab=0, n_arriving=bs // 2, pool_blocks=None)
+    arriving = np.arange(bs) % 2 == 1
+    meta = make_meta(cfg, seq_lens=lens, depth=depth, arriving=arriving)
+    _check_all(cfg, meta, device, split_tokens=split)
+
+
+def test_ragged_batch_of_64(device):
+    rng = np.random.default_rng(5)
+    lens = rng.integers(1, 700, 64)
+    depth = np.minimum(rng.integers(0, 9, 64), lens - 1)
+    cfg = custom_config(seed=7, bs=64, num_q_heads=32, num_kv_heads=8, head_dim=128, vocab=2048,
+                        n_arriving=20, pool_blocks=None, k_lo=0, k_hi=8)
+    meta = make_meta(cfg, seq_lens=lens, depth=depth)
+    _check_all(cfg, meta, device)
+    _check_all(cfg, meta, device, split_tokens=64)
+
+
+def test_multi_layer_gather_subrange(device):
+    cfg = custom_config(seed=3, num_layers=3)
+    meta = make_meta(cfg)
+    layers = [make_layer(cfg, meta, l, "cpu") for l in range(3)]
+    stack = lambda name: torch.stack([getattr(l, name) for l in layers]).to(device).contiguous()
+    kp, vp, ks, vs = (stack(n) for n in ("k_pool", "v_pool", "k_stage", "v_stage"))
+    nsd.kv_gather(ks, vs, kp, vp, i32(meta.src_ids, device), i32(meta.dst_ids, device),
+                  layer0=1, n_layers=1)
+    torch.cuda.synchronize()
+    ref_k, ref_v = oracle.gather.kv_gather(
+        np.stack([u16(l.k_stage) for l in layers]), np.stack([u16(l.v_stage) for l in layers]),
+        np.stack([u16(l.k_pool) for l in layers]), np.stack([u16(l.v_pool) for l in layers]),
+        meta.src_ids, meta.dst_ids, layer0=1, n_layers=1)
+    assert np.array_equal(u16(kp), ref_k) and np.array_equal(u16(vp), ref_v)
+
+
+def test_gather_empty_plan_and_idempotence(device):
+    cfg = CONFIGS["tiny"]
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
+    ks, vs = lay.k_stage.to(device), lay.v_stage.to(device)
+    e = torch.zeros(0, dtype=torch.int32, device=device)
+    nsd.kv_gather(ks, vs, kp, vp, e, e)
+    torch.cuda.synchronize()
+    assert np.array_equal(u16(kp), u16(lay.k_pool))
+    src, dst = i32(meta.src_ids, device), i32(meta.dst_ids, device)
+    nsd.kv_gather(ks, vs, kp, vp, src, dst)
+    once = u16(kp).copy()
+    nsd.kv_gather(ks, vs, kp, vp, src, dst)
+    assert np.array_equal(u16(kp), once)
+
+
+def test_attention_deterministic_and_permutation_invariant(device):
+    cfg = custom_config(seed=21, bs=6, num_q_heads=32, num_kv_heads=8, head_dim=128, vocab=0,
+                        ctx_lo=200, ctx_hi=900, n_arriving=0, pool_blocks=None)
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    q = lay.q.to(device)
+    args = (i32(meta.seq_lens, device), i32(meta.q_indptr, device), meta.max_q, meta.max_seq_len)
+    kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
+    bt = i32(meta.block_table, device)
+    o1 = nsd.verify_attention(q, kp, vp, bt, *args).clone()
+    o2 = nsd.verify_attention(q, kp, vp, bt, *args).clone()
+    # same logical cache under a different physical placement
+    sigma = np.random.default_rng(1).permutation(meta.num_blocks)
+    kp2, vp2 = torch.empty_like(kp), torch.empty_like(vp)
+    sig = torch.as_tensor(sigma, device=device)
+    kp2[sig] = kp
+    vp2[sig] = vp
+    bt2 = np.where(meta.block_table >= 0, sigma[np.maximum(meta.block_table, 0)], -1)
+    o3 = nsd.verify_attention(q, kp2, vp2, i32(bt2, device), *args)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(o1.view(torch.int16), o3.view(torch.int16))
+    check_attention(meta, lay, o1, range(cfg.bs))
+
+
+def test_out_of_range_block_ids_are_invisible(device):
+    # a block id past the pool makes its tokens invisible; nothing faults
+    cfg = custom_config(seed=31, bs=2, vocab=0, n_arriving=0, ctx_lo=64, ctx_hi=64, k_lo=0, k_hi=0,
+                        pool_blocks=None)
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    bt = meta.block_table.copy()
+    bt[1, 3] = meta.num_blocks + 1000   # last block of request 1: its 16 tokens vanish
+    out = nsd.verify_attention(lay.q.to(device), lay.k_pool.to(device), lay.v_pool.to(device),
+                               i32(bt, device), i32(meta.seq_lens, device),
+                               i32(meta.q_indptr, device), 1, 64)
+    torch.cuda.synchronize()
+    check_attention(meta, lay, out, [0])
+    # request 1's only query (position 63) lives in the dropped block: it sees tokens 0..47
+    from workload.synth import logical_kv
+    k, v = logical_kv(meta, lay, 1)
+    qr = lay.q[1:2].double().numpy()
+    ref = oracle.attention.verify_attention_request(qr, k[:48].double().numpy(),
+                                                    v[:48].double().numpy(), 0.125)
+    # the oracle places the query at the last visible position, which is the same set of keys
+    assert np.abs(out[1:2].float().cpu().numpy() - ref).max() <= 2e-2
+
+
+# ---------------------------------------------------------------- acceptance
+
+def _accept(dev, p, q, x, u, q_indptr, max_k):
+    t = lambda a, dt: torch.as_tensor(np.ascontiguousarray(a), dtype=dt, device=dev)
+    acc, tok = nsd.spec_accept(t(p, torch.float32), t(q, torch.float32) if max_k else None,
+                               t(x, torch.int32) if max_k else None, t(u, torch.float32),
+                               t(q_indptr, torch.int32), max_k)
+    torch.cuda.synchronize()
+    return acc.cpu().numpy(), tok.cpu().numpy()
+
+
+def _probs(rng, rows, vocab, sigma=2.0):
+    z = sigma * rng.standard_normal((rows, vocab))
+    e = np.exp(z - z.max(1, keepdims=True))
+    return (e / e.sum(1, keepdims=True)).astype(np.float32)
+
+
+def _batch(depth):
+    q_indptr = np.concatenate([[0], np.cumsum(np.array(depth) + 1)]).astype(np.int32)
+    return q_indptr, int(q_indptr[-1]), len(depth)
+
+
+def test_accept_random_ragged(device):
+    rng = np.random.default_rng(0)
+    depth = rng.integers(0, 9, 300)
+    q_indptr, tq, bs = _batch(depth)
+    vocab = 4096
+    p = _probs(rng, tq, vocab, 1.0)
+    q = _probs(rng, tq - bs, vocab, 1.0)
+    x = np.array([rng.choice(vocab, p=row.astype(np.float64) / row.astype(np.float64).sum())
+                  for row in q], dtype=np.int32)
+    u = (rng.integers(0, 1 << 24, tq) * 2.0**-24).astype(np.float32)
+    acc, tok = _accept(device, p, q, x, u, q_indptr, 8)
+    check_accept(p, q, x, u, q_indptr, acc, tok)
+    assert acc.max() >= 2   # some requests accept several proposals
+
+
+def test_accept_identical_rows_accept_all(device):
+    rng = np.random.default_rng(1)
+    depth = [4] * 16
+    q_indptr, tq, bs = _batch(depth)
+    p = _probs(rng, tq, 1000)
+    q = np.concatenate([p[q_indptr[r]:q_indptr[r] + 4] for r in range(bs)])
+    x = rng.integers(0, 1000, tq - bs).astype(np.int32)
+    u = (rng.integers(0, 1 << 24, tq) * 2.0**-24).astype(np.float32)
+    acc, tok = _accept(device, p, q, x, u, q_indptr, 4)
+    assert np.all(acc == 4)
+    check_accept(p, q, x, u, q_indptr, acc, tok)
+
+
+def test_accept_special_cases(device):
+    vocab = 16
+    depth = [1, 1, 1, 0, 2]
+    q_indptr, tq, bs = _batch(depth)
+    p = np.full((tq, vocab), 1.0 / vocab, np.float32)
+    q = np.full((tq - bs, vocab), 1.0 / vocab, np.float32)
+    x = np.zeros(tq - bs, np.int32)
+    u = np.full(tq, 0.5, np.float32)
+    # r0: one-hot residual forced: proposal 3 has p = 0, p_0 one-hot at 9
+    a = q_indptr[0]
+    p[a] = 0
+    p[a, 9] = 1.0
+    x[0] = 3
+    # r1: out-of-vocabulary proposal with p_0 = q_0: rejected, residual empty -> draw from p_0
+    x[1] = vocab + 5
+    # r2: exact tie u*q = p -> accepted; bonus from p_1 one-hot at 12
+    a = q_indptr[2]
+    q[2] = 0
+    q[2, 7] = 0.5
+    p[a] = 0
+    p[a, 7] = 0.25
+    p[a, 1] = 0.75
+    x[2] = 7
+    p[a + 1] = 0
+    p[a + 1, 12] = 1.0
+    # r3: K = 0: plain draw from p_0 at u = 1 - 2^-24 -> the last token of weight
+    a = q_indptr[3]
+    p[a] = 0
+    p[a, 2] = 0.5
+    p[a, 5] = 0.5
+    u[a] = np.float32(1 - 2**-24)
+    # r4: u exactly on a CDF boundary of exactly representable weights
+    a = q_indptr[4]
+    x[3], x[4] = 0, 1
+    p[a + 2] = np.array([0.25, 0.25, 0, 0.5] + [0] * 12, np.float32)
+    u[a + 2] = 0.25
+    acc, tok = _accept(device, p, q, x, u, q_indptr, 2)
+    assert list(acc) == [0, 0, 1, 0, 2]
+    assert tok[q_indptr[0]] == 9
+    assert tok[q_indptr[2]:q_indptr[2] + 2].tolist() == [7, 12]
+    assert tok[q_indptr[3]] == 5
+    assert tok[q_indptr[4] + 2] == 1
+    check_accept(p, q, x, u, q_indptr, acc, tok)
+
+
+def test_first_token_follows_target_row(device):
+    # speculative-sampling theorem on the GPU: 200k requests share (p_0, q_0)
+    from scipy import stats
+    rng = np.random.default_rng(3)
+    vocab, bs = 8, 200000
+    p0 = _probs(rng, 1, vocab, 1.0)[0]
+    q0 = _probs(rng, 1, vocab, 1.0)[0]
+    p1 = _probs(rng, 1, vocab, 1.0)[0]
+    q_indptr, tq, _ = _batch([1] * bs)
+    p = np.tile(np.stack([p0, p1]), (bs, 1))
+    q = np.tile(q0[None], (bs, 1))
+    qq = q0.astype(np.float64)
+    x = rng.choice(vocab, size=bs, p=qq / qq.sum()).astype(np.int32)
+    u = (rng.integers(0, 1 << 24, tq) * 2.0**-24).astype(np.float32)
+    acc, tok = _accept(device, p, q, x, u, q_indptr, 1)
+    counts = np.bincount(tok[q_indptr[:-1]], minlength=vocab)
+    r64 = p0.astype(np.float64)
+    assert stats.chisquare(counts, r64 / r64.sum() * bs).pvalue > 1e-4
+    check_accept(p, q, x, u, q_indptr, acc, tok, requests=range(0, bs, 97))
