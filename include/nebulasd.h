@@ -99,8 +99,11 @@ nsd_status nsd_kv_gather(const void* src_k, const void* src_v, int64_t src_num_b
                          void* stream);
 
 /*
- * Bytes of workspace nsd_verify_attention needs for these sizes (0 if the
- * sizes are invalid).  Depends only on its arguments.
+ * Bytes of workspace nsd_verify_attention needs for these sizes on the
+ * current HIP device (0 if the sizes are invalid).  The size depends on the
+ * arguments and on how many waves the device keeps resident (its CU count);
+ * the environment variable NSD_ATTN_WAVES (a positive multiple of 4), if set,
+ * overrides that wave count for both this query and the launch.
  */
 size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
                                            int32_t num_kv_heads, int32_t head_dim,

@@ -4,7 +4,7 @@
 #include <stdint.h>
 #include <stdio.h>
 #include <stdarg.h>
-#include "../../include/nebulasd.h"
+#include "nebulasd.h"
 
 namespace nsd {
 

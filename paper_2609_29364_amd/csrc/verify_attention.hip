@@ -4,9 +4,8 @@
 // append-dominant cache that already holds the window).
 //
 // Design (gfx950, wave64, bf16 MFMA 16x16x32):
-// * Work item = (request r, KV head g, context split).  One wave owns an item;
-//   the (Hq/Hkv) query heads x n_q queries that share KV head g form the M
-//   rows of its tile products, so each K/V byte is read from HBM once for the
+// * The (Hq/Hkv) query heads x n_q queries that share KV head g form the M rows
+//   of one wave's tile products, so each K/V byte is read from HBM once for the
 //   whole group.
 // * S^T = K Q^T: the K plane's [D/8][16][8] run layout puts, for MFMA k-step
 //   kk, the 16 slots x 8 dims that lane group (lane/16) needs in one 256-byte
@@ -19,13 +18,13 @@
 //   contiguous per instruction), and P^T is exactly the S^T accumulator
 //   layout (converted to bf16), with no data exchange between lanes.  O^T
 //   accumulates per lane for one query row, so the online-softmax rescale is
-//   lane-local.
-// * Two 16-token blocks (a 32-token span) per step; the next span's loads are
-//   issued before the current span's math (register double buffering).
-// * Long contexts are cut into splits of `split_tokens`; each split writes
-//   (O unnormalised, running max, sum) partials and a second kernel merges
-//   them in split order (deterministic, no atomics).  A request that fits one
-//   split writes its output directly.
+//   lane-local.  No LDS round trip is needed for either operand.
+// * K/V are streamed once, so they are loaded non-temporally.
+// * Load balance (stream-K): the spans of all (request, KV head) items are cut
+//   into as many equal contiguous ranges as the device keeps waves resident,
+//   whatever the spread of context lengths.  Items cut by a range boundary
+//   leave partials that a small second kernel merges in wave order
+//   (deterministic, no atomics); all other items are written directly.
 // * Masked tokens (past a query's position, past L_r, or in a block whose id
 //   is out of range) are removed by selection: scores become -inf and V
 //   elements past L_r are zeroed, so NaN-filled unused slots never leak.
@@ -54,18 +53,18 @@ struct Params {
   const int32_t* seq_lens;
   const int32_t* q_indptr;
   uint16_t* out;
-  float* part_o;     // [bs][Hkv][max_splits][MT*16][D]
-  float2* part_ml;   // [bs][Hkv][max_splits][MT*16]: (running max, sum)
+  float* part_o;     // [2 * num_waves][MT*16][D]: head/tail partial O per wave
+  float2* part_ml;   // [2 * num_waves][MT*16]: (running max, sum)
+  int64_t* prefix;   // [bs+1]: exclusive prefix of per-request span counts
   int64_t num_blocks;
+  int32_t bs;
   int32_t max_blocks_per_seq;
   int32_t num_q_heads;
   int32_t num_kv_heads;
   int32_t group;
   int32_t max_q;
   int32_t max_seq_len;
-  int32_t split_tokens;
-  int32_t max_splits;
-  int32_t waves_per_wg;
+  int32_t num_waves;
   float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -113,14 +112,14 @@ __device__ inline void issue_span(Span<D>& s, const Params& p, const int32_t* bt
 #pragma unroll
   for (int kk = 0; kk < D / 32; ++kk) {
     const int off = ((kk * 4 + grp) * kBlock + row) * 8;
-    s.k[0][kk] = *(const u32x4*)(k0 + off);
-    s.k[1][kk] = *(const u32x4*)(k1 + off);
+    s.k[0][kk] = __builtin_nontemporal_load((const u32x4*)(k0 + off));
+    s.k[1][kk] = __builtin_nontemporal_load((const u32x4*)(k1 + off));
   }
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) {
     const int off = (dt * 16 + row) * kBlock + grp * 4;
-    s.v[0][dt] = *(const u32x2*)(v0 + off);
-    s.v[1][dt] = *(const u32x2*)(v1 + off);
+    s.v[0][dt] = __builtin_nontemporal_load((const u32x2*)(v0 + off));
+    s.v[1][dt] = __builtin_nontemporal_load((const u32x2*)(v1 + off));
   }
 }
 
@@ -211,140 +210,235 @@ __device__ inline void compute_span(const Span<D>& s, const bf16x8 (&qop)[MT][D 
   }
 }
 
-template <int D, int MT, bool PREFETCH>
-__global__ __launch_bounds__(256) void verify_attention_kernel(Params p) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+__device__ inline int clamp_len(const Params& p, int r) {
+  const int L = p.seq_lens[r];
+  return max(0, min(L, min(p.max_seq_len, p.max_blocks_per_seq * kBlock)));
+}
+
+// Spans of one (request, KV head) item; an empty context still owns one span
+// so that its rows are written (as zeros).
+__device__ inline int spans_of(int L) { return max(1, (L + kSpan - 1) / kSpan); }
+
+__device__ inline int64_t wave_sum_i64(int64_t x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+__device__ inline int64_t wave_incl_scan_i64(int64_t x, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// First span of wave w's range of the T global spans split over W waves.
+__device__ inline int64_t range_start(int64_t w, int64_t total, int64_t waves) {
+  return w * total / waves;
+}
+
+// The wave whose range holds global span s.
+__device__ inline int64_t wave_of(int64_t s, int64_t total, int64_t waves) {
+  return ((s + 1) * waves - 1) / total;
+}
+
+// Stream-K decomposition: the global sequence of spans, ordered by request,
+// then KV head, then position, is cut into W equal contiguous ranges, one per
+// resident wave.  A wave runs the online softmax over every (request, KV head)
+// item its range touches; an item wholly inside the range is finished and
+// written directly, an item cut by a range boundary leaves a partial (running
+// max, sum, unnormalised O) in the wave's head slot (item began in an earlier
+// range) or tail slot (item continues in a later range) for the merge kernel.
+template <int D, int MT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT <= 2 ? 2 : 1)))
+void verify_attention_kernel(Params p) {
+  __shared__ int64_t s_wsum[4];
+  __shared__ int s_r0[4];
+  __shared__ int64_t s_p0[4];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int grp = lane >> 4;
-  const int split = blockIdx.x;
-  const int g = blockIdx.y * p.waves_per_wg + wave;
-  const int r = blockIdx.z;
+  const int64_t W = p.num_waves;
+  const int hkv = p.num_kv_heads;
 
-  int L = p.seq_lens[r];
-  L = max(0, min(L, min(p.max_seq_len, p.max_blocks_per_seq * kBlock)));
-  const int qo = p.q_indptr[r];
-  const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
-  if (nq == 0) return;
-  const int nsplit = L > 0 ? (L + p.split_tokens - 1) / p.split_tokens : 1;
-  if (split >= nsplit) return;
-  const int t0 = split * p.split_tokens;
-  const int t1 = min(L, t0 + p.split_tokens);
-  const int rows = p.group * nq;
-  const int win = L - nq;   // position of the anchor query
-
-  bf16x8 qop[MT][D / 32];
-  int pos[MT];
+  // total spans T
+  int64_t local = 0;
+  for (int r = tid; r < p.bs; r += 256) local += spans_of(clamp_len(p, r));
+  local = wave_sum_i64(local);
+  if (lane == 0) s_wsum[wave] = local;
+  if (tid < 4) s_r0[tid] = -1;
+  __syncthreads();
+  const int64_t T = (s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3]) * hkv;
+  int64_t ws0[4];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = mt * 16 + (lane & 15);
-    if (m < rows) {
-      const int j = m / p.group;
-      const int h = g * p.group + m % p.group;
-      const uint16_t* src = p.q + ((int64_t)(qo + j) * p.num_q_heads + h) * D;
-#pragma unroll
-      for (int kk = 0; kk < D / 32; ++kk)
-        qop[mt][kk] = __builtin_bit_cast(bf16x8, *(const u32x4*)(src + kk * 32 + grp * 8));
-      pos[mt] = win + j;
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < D / 32; ++kk) qop[mt][kk] = bf16x8{};
-      pos[mt] = L - 1;
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int64_t w = (int64_t)blockIdx.x * 4 + i;
+    ws0[i] = range_start(w, T, W);
+    if (tid == 0 && (w >= W || ws0[i] >= range_start(w + 1, T, W))) s_r0[i] = -2;  // empty
   }
-
-  f32x4 acc[MT][D / 16];
-  float m_run[MT], l_run[MT];
+  // exclusive prefix of per-request span counts; locate each wave's first request
+  int64_t carry = 0;
+  for (int base = 0; base < p.bs; base += 256) {
+    const int r = base + tid;
+    const int64_t n = r < p.bs ? spans_of(clamp_len(p, r)) : 0;
+    const int64_t incl = wave_incl_scan_i64(n, lane);
+    __syncthreads();
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int64_t before = carry;
+    for (int i = 0; i < wave; ++i) before += s_wsum[i];
+    const int64_t excl = before + incl - n;
+    if (r < p.bs) {
+      if (blockIdx.x == 0) p.prefix[r] = excl;
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    m_run[mt] = -INFINITY;
-    l_run[mt] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) acc[mt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  const int32_t* bt = p.block_table + (int64_t)r * p.max_blocks_per_seq;
-  const int n_span = (t1 - t0 + kSpan - 1) / kSpan;
-  if constexpr (PREFETCH) {
-    // register double buffering: the next span's loads fly during this span's math
-    Span<D> a, b;
-    if (n_span > 0) issue_span<D>(a, p, bt, g, t0, L, lane);
-    for (int si = 0; si < n_span; si += 2) {
-      if (si + 1 < n_span) issue_span<D>(b, p, bt, g, t0 + (si + 1) * kSpan, L, lane);
-      compute_span<D, MT>(a, qop, acc, m_run, l_run, pos, L, win, p.scale_log2, lane);
-      if (si + 1 >= n_span) break;
-      if (si + 2 < n_span) issue_span<D>(a, p, bt, g, t0 + (si + 2) * kSpan, L, lane);
-      compute_span<D, MT>(b, qop, acc, m_run, l_run, pos, L, win, p.scale_log2, lane);
+      for (int i = 0; i < 4; ++i)
+        if (hkv * excl <= ws0[i] && ws0[i] < hkv * (excl + n)) {
+          s_r0[i] = r;
+          s_p0[i] = excl;
+        }
     }
-  } else {
-    // one span buffer; latency is hidden by the other resident waves
-    for (int si = 0; si < n_span; ++si) {
-      Span<D> a;
-      issue_span<D>(a, p, bt, g, t0 + si * kSpan, L, lane);
-      compute_span<D, MT>(a, qop, acc, m_run, l_run, pos, L, win, p.scale_log2, lane);
-    }
+    carry += s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
+    __syncthreads();
+    const bool found = s_r0[0] != -1 && s_r0[1] != -1 && s_r0[2] != -1 && s_r0[3] != -1;
+    if (blockIdx.x != 0 && found) break;
   }
+  if (blockIdx.x == 0 && tid == 0) p.prefix[p.bs] = carry;
+  __syncthreads();
 
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) l_run[mt] = wave_sum_groups(l_run[mt]);
+  const int64_t w = (int64_t)blockIdx.x * 4 + wave;
+  int r = s_r0[wave];
+  if (r < 0) return;
+  int64_t pr = s_p0[wave];
+  int64_t s = ws0[wave];
+  const int64_t s1 = range_start(w + 1, T, W);
 
-  if (nsplit == 1) {
+  while (s < s1) {
+    const int L = clamp_len(p, r);
+    const int n = spans_of(L);
+    const int qo = p.q_indptr[r];
+    const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
+    const int64_t off = s - hkv * pr;
+    const int g = (int)(off / n);
+    const int j0 = (int)(off - (int64_t)g * n);
+    const int j1 = (int)min((int64_t)n, j0 + (s1 - s));
+    const int rows = p.group * nq;
+    const int win = L - nq;
+
+    bf16x8 qop[MT][D / 32];
+    int pos[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = mt * 16 + (lane & 15);
-      if (m >= rows) continue;
-      const int j = m / p.group;
-      const int h = g * p.group + m % p.group;
-      const float inv = l_run[mt] > 0.f ? 1.f / l_run[mt] : 0.f;
-      uint16_t* dst = p.out + ((int64_t)(qo + j) * p.num_q_heads + h) * D + grp * 4;
+      if (m < rows) {
+        const int j = m / p.group;
+        const int h = g * p.group + m % p.group;
+        const uint16_t* src = p.q + ((int64_t)(qo + j) * p.num_q_heads + h) * D;
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const bf16x2 lo = {(__bf16)(acc[mt][dt][0] * inv), (__bf16)(acc[mt][dt][1] * inv)};
-        const bf16x2 hi = {(__bf16)(acc[mt][dt][2] * inv), (__bf16)(acc[mt][dt][3] * inv)};
-        *(u32x2*)(dst + dt * 16) = u32x2{__builtin_bit_cast(uint32_t, lo),
-                                         __builtin_bit_cast(uint32_t, hi)};
+        for (int kk = 0; kk < D / 32; ++kk)
+          qop[mt][kk] = __builtin_bit_cast(bf16x8, *(const u32x4*)(src + kk * 32 + grp * 8));
+        pos[mt] = win + j;
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < D / 32; ++kk) qop[mt][kk] = bf16x8{};
+        pos[mt] = L - 1;
       }
     }
-  } else {
-    const int64_t item = ((int64_t)r * p.num_kv_heads + g) * p.max_splits + split;
+    f32x4 acc[MT][D / 16];
+    float m_run[MT], l_run[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const int m = mt * 16 + (lane & 15);
-      if (m >= rows) continue;
-      float* dst = p.part_o + (item * (MT * 16) + m) * D + grp * 4;
+      m_run[mt] = -INFINITY;
+      l_run[mt] = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) *(f32x4*)(dst + dt * 16) = acc[mt][dt];
-      if (grp == 0) p.part_ml[item * (MT * 16) + m] = make_float2(m_run[mt], l_run[mt]);
+      for (int dt = 0; dt < D / 16; ++dt) acc[mt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const int32_t* bt = p.block_table + (int64_t)r * p.max_blocks_per_seq;
+    for (int j = j0; j < j1; ++j) {
+      Span<D> sp;
+      issue_span<D>(sp, p, bt, g, j * kSpan, L, lane);
+      compute_span<D, MT>(sp, qop, acc, m_run, l_run, pos, L, win, p.scale_log2, lane);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) l_run[mt] = wave_sum_groups(l_run[mt]);
+
+    if (j0 == 0 && j1 == n) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mt * 16 + (lane & 15);
+        if (m >= rows) continue;
+        const int j = m / p.group;
+        const int h = g * p.group + m % p.group;
+        const float inv = l_run[mt] > 0.f ? 1.f / l_run[mt] : 0.f;
+        uint16_t* dst = p.out + ((int64_t)(qo + j) * p.num_q_heads + h) * D + grp * 4;
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) {
+          const bf16x2 lo = {(__bf16)(acc[mt][dt][0] * inv), (__bf16)(acc[mt][dt][1] * inv)};
+          const bf16x2 hi = {(__bf16)(acc[mt][dt][2] * inv), (__bf16)(acc[mt][dt][3] * inv)};
+          *(u32x2*)(dst + dt * 16) = u32x2{__builtin_bit_cast(uint32_t, lo),
+                                           __builtin_bit_cast(uint32_t, hi)};
+        }
+      }
+    } else {
+      const int64_t slot = 2 * w + (j0 > 0 ? 0 : 1);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mt * 16 + (lane & 15);
+        if (m >= rows) continue;
+        float* dst = p.part_o + (slot * (MT * 16) + m) * D + grp * 4;
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) *(f32x4*)(dst + dt * 16) = acc[mt][dt];
+        if (grp == 0) p.part_ml[slot * (MT * 16) + m] = make_float2(m_run[mt], l_run[mt]);
+      }
+    }
+    s += j1 - j0;
+    if (j1 == n && g == hkv - 1) {
+      pr += n;
+      ++r;
     }
   }
 }
 
-// Merge split partials of one (request, KV head) in split order.
+// Merge the partials of every item that a range boundary cut, in wave order
+// (deterministic, no atomics).
 template <int D, int MT>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const int g = blockIdx.x;
   const int r = blockIdx.y;
-  int L = p.seq_lens[r];
-  L = max(0, min(L, min(p.max_seq_len, p.max_blocks_per_seq * kBlock)));
+  const int hkv = p.num_kv_heads;
+  const int64_t W = p.num_waves;
+  const int64_t T = p.prefix[p.bs] * hkv;
+  const int L = clamp_len(p, r);
+  const int n = spans_of(L);
   const int qo = p.q_indptr[r];
   const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
-  const int nsplit = L > 0 ? (L + p.split_tokens - 1) / p.split_tokens : 1;
-  if (nq == 0 || nsplit <= 1) return;
+  const int64_t a = p.prefix[r] * hkv + (int64_t)g * n;
+  const int64_t wa = wave_of(a, T, W);
+  const int64_t wb = wave_of(a + n - 1, T, W);
+  if (wa == wb || nq == 0) return;
   const int rows = p.group * nq;
-  const int64_t item0 = ((int64_t)r * p.num_kv_heads + g) * p.max_splits;
   constexpr int kVec = D / 4;
   for (int idx = threadIdx.x; idx < rows * kVec; idx += blockDim.x) {
     const int m = idx / kVec;
     const int d = (idx % kVec) * 4;
     float mx = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, p.part_ml[(item0 + s) * (MT * 16) + m].x);
+    for (int64_t w = wa; w <= wb; ++w) {
+      if (w > wa && range_start(w, T, W) == range_start(w + 1, T, W)) continue;
+      const int64_t slot = 2 * w + (w == wa ? 1 : 0);
+      mx = fmaxf(mx, p.part_ml[slot * (MT * 16) + m].x);
+    }
     f32x4 num = {0.f, 0.f, 0.f, 0.f};
     float den = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-      const float2 ml = p.part_ml[(item0 + s) * (MT * 16) + m];
-      const float w = (ml.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml.x - mx);
-      const f32x4 o = *(const f32x4*)(p.part_o + ((item0 + s) * (MT * 16) + m) * D + d);
-      num += w * o;
-      den += w * ml.y;
+    for (int64_t w = wa; w <= wb; ++w) {
+      if (w > wa && range_start(w, T, W) == range_start(w + 1, T, W)) continue;
+      const int64_t slot = 2 * w + (w == wa ? 1 : 0);
+      const float2 ml = p.part_ml[slot * (MT * 16) + m];
+      const float wt = (ml.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml.x - mx);
+      const f32x4 o = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
+      num += wt * o;
+      den += wt * ml.y;
     }
     const float inv = den > 0.f ? 1.f / den : 0.f;
     const int j = m / p.group;
@@ -356,32 +450,53 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   }
 }
 
+template <int D, int MT>
+const void* kernel_ptr() {
+  return (const void*)&verify_attention_kernel<D, MT>;
+}
+
+const void* kernel_for(int d, int mt) {
+  if (d == 64) {
+    switch (mt) {
+      case 1: return kernel_ptr<64, 1>();
+      case 2: return kernel_ptr<64, 2>();
+      case 3: return kernel_ptr<64, 3>();
+      default: return kernel_ptr<64, 4>();
+    }
+  }
+  switch (mt) {
+    case 1: return kernel_ptr<128, 1>();
+    case 2: return kernel_ptr<128, 2>();
+    case 3: return kernel_ptr<128, 3>();
+    default: return kernel_ptr<128, 4>();
+  }
+}
+
 struct Plan {
   int mt;            // 16-row tiles
-  int split_tokens;
-  int max_splits;
-  size_t ws_bytes;
+  int num_waves;     // W: resident waves of the launch
+  size_t prefix_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
 };
 
-// Split length: the longest power-of-two multiple of 32 tokens that still
-// gives the launch at least kMinItems (request, KV head, split) items, so the
-// 256 CUs stay busy with ragged contexts, while long splits keep the partial
-// traffic small.
-int choose_split_tokens(int bs, int hkv, int max_seq_len) {
-  const char* env = getenv("NSD_SPLIT_TOKENS");
+// Waves the device keeps resident for this kernel (CUs x waves per CU), or
+// NSD_ATTN_WAVES when set (a multiple of 4, for tests and tuning).
+int resident_waves(int d, int mt) {
+  const char* env = getenv("NSD_ATTN_WAVES");
   if (env) {
     const int v = atoi(env);
-    if (v >= kSpan && v % kSpan == 0) return v;
+    if (v >= 4 && v % 4 == 0) return v;
   }
-  constexpr int64_t kMinItems = 8192;
-  int s = kSpan;
-  while (s < max_seq_len) {
-    const int64_t next = 2 * (int64_t)s;
-    const int64_t items = (int64_t)bs * hkv * ((max_seq_len + next - 1) / next);
-    if (items < kMinItems) break;
-    s = (int)next;
+  int dev = 0, cus = 0, blocks = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel_for(d, mt), 256, 0) !=
+          hipSuccess ||
+      cus <= 0 || blocks <= 0) {
+    (void)hipGetLastError();
+    cus = 256;
+    blocks = 2;
   }
-  return s;
+  return cus * blocks * 4;
 }
 
 bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, Plan* pl) {
@@ -391,35 +506,20 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, Plan*
   const int rows = (hq / hkv) * max_q;
   if (rows > kMaxRows) return false;
   pl->mt = (rows + 15) / 16;
-  pl->split_tokens = choose_split_tokens(bs, hkv, max_seq_len);
-  pl->max_splits = max(1, (max_seq_len + pl->split_tokens - 1) / pl->split_tokens);
-  if (pl->max_splits == 1) {
-    pl->ws_bytes = 0;
-  } else {
-    const size_t items = (size_t)bs * hkv * pl->max_splits * pl->mt * 16;
-    pl->ws_bytes = items * (size_t)d * sizeof(float) + items * sizeof(float2);
-  }
+  pl->num_waves = resident_waves(d, pl->mt);
+  const size_t slots = 2 * (size_t)pl->num_waves * pl->mt * 16;
+  pl->prefix_bytes = (((size_t)bs + 1) * sizeof(int64_t) + 255) / 256 * 256;
+  pl->part_o_bytes = slots * d * sizeof(float);
+  pl->part_ml_bytes = slots * sizeof(float2);
+  pl->ws_bytes = pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes;
   return true;
-}
-
-bool use_prefetch(int d, int mt) {
-  const char* env = getenv("NSD_ATTN_PREFETCH");
-  if (env) return atoi(env) != 0;
-  return d == 64 ? mt <= 2 : mt <= 1;
 }
 
 template <int D, int MT>
 void launch(const Params& p, int bs, hipStream_t stream) {
-  dim3 grid(p.max_splits, p.num_kv_heads / p.waves_per_wg, bs);
-  if (MT <= 2 && use_prefetch(D, MT))
-    hipLaunchKernelGGL((verify_attention_kernel<D, MT, MT <= 2>), grid, dim3(64 * p.waves_per_wg),
-                       0, stream, p);
-  else
-    hipLaunchKernelGGL((verify_attention_kernel<D, MT, false>), grid, dim3(64 * p.waves_per_wg),
-                       0, stream, p);
-  if (p.max_splits > 1)
-    hipLaunchKernelGGL((combine_kernel<D, MT>), dim3(p.num_kv_heads, bs), dim3(256), 0, stream,
-                       p);
+  hipLaunchKernelGGL((verify_attention_kernel<D, MT>), dim3(p.num_waves / 4), dim3(256), 0,
+                     stream, p);
+  hipLaunchKernelGGL((combine_kernel<D, MT>), dim3(p.num_kv_heads, bs), dim3(256), 0, stream, p);
 }
 
 template <int D>
@@ -478,7 +578,7 @@ extern "C" nsd_status nsd_verify_attention(const void* q, const void* k_cache,
     return fail(NSD_ERR_NULL, "verify_attention: NULL pointer argument");
   Plan pl;
   make_plan(bs, num_q_heads, num_kv_heads, head_dim, max_q_per_seq, max_seq_len, &pl);
-  if (pl.ws_bytes > 0 && (!workspace || workspace_bytes < pl.ws_bytes))
+  if (!workspace || workspace_bytes < pl.ws_bytes)
     return fail(NSD_ERR_WORKSPACE, "verify_attention: workspace of %zu bytes needed, %zu given",
                 pl.ws_bytes, workspace ? workspace_bytes : (size_t)0);
 
@@ -490,19 +590,18 @@ extern "C" nsd_status nsd_verify_attention(const void* q, const void* k_cache,
   p.seq_lens = seq_lens;
   p.q_indptr = q_indptr;
   p.out = (uint16_t*)out;
-  const size_t items = (size_t)bs * num_kv_heads * pl.max_splits * pl.mt * 16;
-  p.part_o = (float*)workspace;
-  p.part_ml = pl.ws_bytes ? (float2*)((char*)workspace + items * head_dim * sizeof(float)) : nullptr;
+  p.prefix = (int64_t*)workspace;
+  p.part_o = (float*)((char*)workspace + pl.prefix_bytes);
+  p.part_ml = (float2*)((char*)workspace + pl.prefix_bytes + pl.part_o_bytes);
   p.num_blocks = num_blocks;
+  p.bs = bs;
   p.max_blocks_per_seq = max_blocks_per_seq;
   p.num_q_heads = num_q_heads;
   p.num_kv_heads = num_kv_heads;
   p.group = num_q_heads / num_kv_heads;
   p.max_q = max_q_per_seq;
   p.max_seq_len = max_seq_len;
-  p.split_tokens = pl.split_tokens;
-  p.max_splits = pl.max_splits;
-  p.waves_per_wg = num_kv_heads % 4 == 0 ? 4 : (num_kv_heads % 2 == 0 ? 2 : 1);
+  p.num_waves = pl.num_waves;
   p.scale_log2 = scale * 1.4426950408889634f;
 
   clear_stale_error();

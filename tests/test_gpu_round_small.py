@@ -1,6 +1,8 @@
 """GPU parity on small rounds: every step against the oracle, element by element,
 plus edge cases (ragged depths, L mod 16 in {0, 1, 15}, L = n_q, every GQA
-group size, both head dims, forced context splits)."""
+group size, both head dims).  The attention's work decomposition is forced
+through few waves (most items whole) and the device's full wave count (most
+items cut into partials) via NSD_ATTN_WAVES."""
 import os
 
 import numpy as np
@@ -16,7 +18,7 @@ from parity import i32, u16, check_attention, check_accept
 pytestmark = pytest.mark.gpu
 
 
-def _run_round(cfg, meta, dev, layers=None, accept=True, split_tokens=None):
+def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None):
     layers = layers or [make_layer(cfg, meta, l, "cpu") for l in range(cfg.num_layers)]
     stack = lambda name: torch.stack([getattr(l, name) for l in layers]).to(dev).contiguous()
     kp, vp, ks, vs, q = (stack(n) for n in ("k_pool", "v_pool", "k_stage", "v_stage", "q"))
@@ -25,9 +27,9 @@ def _run_round(cfg, meta, dev, layers=None, accept=True, split_tokens=None):
     if acc_in is not None:
         acc_dev = (acc_in.p_target.to(dev), acc_in.q_draft.to(dev), acc_in.draft_tokens.to(dev),
                    acc_in.uniforms.to(dev), int(meta.depth.max()))
-    old = os.environ.get("NSD_SPLIT_TOKENS")
-    if split_tokens:
-        os.environ["NSD_SPLIT_TOKENS"] = str(split_tokens)
+    old = os.environ.get("NSD_ATTN_WAVES")
+    if waves:
+        os.environ["NSD_ATTN_WAVES"] = str(waves)
     try:
         outs, acc, tok = verify_round(kp, vp, ks, vs, i32(meta.src_ids, dev), i32(meta.dst_ids, dev),
                                       q, i32(meta.block_table, dev), i32(meta.seq_lens, dev),
@@ -35,11 +37,11 @@ def _run_round(cfg, meta, dev, layers=None, accept=True, split_tokens=None):
                                       accept=acc_dev)
         torch.cuda.synchronize()
     finally:
-        if split_tokens:
+        if waves:
             if old is None:
-                del os.environ["NSD_SPLIT_TOKENS"]
+                del os.environ["NSD_ATTN_WAVES"]
             else:
-                os.environ["NSD_SPLIT_TOKENS"] = old
+                os.environ["NSD_ATTN_WAVES"] = old
     return layers, kp, vp, outs, acc_in, acc, tok
 
 
@@ -81,15 +83,15 @@ CASES = [
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
-@pytest.mark.parametrize("split", [None, 32, 96])
-def test_attention_edge_cases(device, case, split):
+@pytest.mark.parametrize("waves", [None, 4, 12])
+def test_attention_edge_cases(device, case, waves):
     hq, hkv, d, lens, depth = CASES[case]
     bs = len(lens)
     cfg = custom_config(seed=100 + case, bs=bs, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
                         vocab=0, n_arriving=bs // 2, pool_blocks=None)
     arriving = np.arange(bs) % 2 == 1
     meta = make_meta(cfg, seq_lens=lens, depth=depth, arriving=arriving)
-    _check_all(cfg, meta, device, split_tokens=split)
+    _check_all(cfg, meta, device, waves=waves)
 
 
 def test_ragged_batch_of_64(device):
@@ -100,7 +102,8 @@ def test_ragged_batch_of_64(device):
                         n_arriving=20, pool_blocks=None, k_lo=0, k_hi=8)
     meta = make_meta(cfg, seq_lens=lens, depth=depth)
     _check_all(cfg, meta, device)
-    _check_all(cfg, meta, device, split_tokens=64)
+    _check_all(cfg, meta, device, waves=8)
+    _check_all(cfg, meta, device, waves=36)
 
 
 def test_multi_layer_gather_subrange(device):
