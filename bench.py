@@ -133,7 +133,7 @@ def main():
     out = torch.empty_like(layer.q)
     ws_n = nsd.verify_attention_workspace_size(cfg.bs, cfg.num_q_heads, cfg.num_kv_heads,
                                                cfg.head_dim, meta.max_q, meta.max_seq_len)
-    ws = torch.empty(max(ws_n, 16), dtype=torch.uint8, device=dev)
+    ws = nsd.new_workspace(ws_n, dev)
     acc_len = torch.empty(cfg.bs, dtype=torch.int32, device=dev)
     toks = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev)

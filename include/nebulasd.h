@@ -137,10 +137,12 @@ size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
  * head_dim in {64, 128}; block_size == 16.
  * scale : the softmax scale (usually 1/sqrt(head_dim)), finite.
  * out : device, bf16 [total_q][num_q_heads][head_dim]; may not alias q or the caches.
- * workspace : device, at least nsd_verify_attention_workspace_size(...) bytes
- *             (may be NULL when that size is 0).  Its contents on entry do not
- *             matter; it is scratch for split partial results.
- * bs == 0 is a no-op returning NSD_OK.
+ * workspace : device, at least nsd_verify_attention_workspace_size(...) bytes.
+ *             Zero-fill it once before its first use; every call leaves it
+ *             ready for the next (a work counter at its start returns to zero
+ *             when the call's kernels end).  Calls sharing a workspace must be
+ *             ordered on one stream.
+ * 1 <= bs <= 8192 (bs == 0 is a no-op returning NSD_OK).
  */
 nsd_status nsd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
                                 int64_t num_blocks, const int32_t* block_table,

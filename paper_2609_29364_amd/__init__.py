@@ -118,6 +118,11 @@ def verify_attention_workspace_size(bs, num_q_heads, num_kv_heads, head_dim, max
                                                          max_q_per_seq, max_seq_len))
 
 
+def new_workspace(nbytes, device):
+    """A verify_attention workspace: zero-filled once, reusable by later calls on its stream."""
+    return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+
+
 def verify_attention(q, k_cache, v_cache, block_table, seq_lens, q_indptr, max_q_per_seq,
                      max_seq_len, scale=None, out=None, workspace=None):
     """One layer of verification attention; returns out [total_q][Hq][D] bf16.
@@ -148,7 +153,7 @@ def verify_attention(q, k_cache, v_cache, block_table, seq_lens, q_indptr, max_q
             raise ValueError("out must have q's shape")
     need = verify_attention_workspace_size(bs, hq, hkv, d, max_q_per_seq, max_seq_len)
     if workspace is None and need:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        workspace = new_workspace(need, q.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check("verify_attention", lib().nsd_verify_attention(
         _ptr(q), _ptr(k_cache), _ptr(v_cache), nb, _ptr(block_table), block_table.shape[1],
@@ -186,4 +191,5 @@ def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, acce
 
 
 __all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
+           "new_workspace",
            "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

@@ -33,6 +33,8 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <algorithm>
+
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
@@ -44,6 +46,7 @@ typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 constexpr int kBlock = 16;   // token slots per KV block
 constexpr int kSpan = 32;    // tokens per main-loop step
 constexpr int kMaxRows = 64; // (Hq/Hkv) * max_q_per_seq limit
+constexpr int kMaxBatch = 8192;   // the span prefix of the batch lives in LDS
 
 struct Params {
   const uint16_t* q;
@@ -55,7 +58,8 @@ struct Params {
   uint16_t* out;
   float* part_o;     // [2 * num_waves][MT*16][D]: head/tail partial O per wave
   float2* part_ml;   // [2 * num_waves][MT*16]: (running max, sum)
-  int64_t* prefix;   // [bs+1]: exclusive prefix of per-request span counts
+  uint32_t* prefix;    // [bs+1]: exclusive prefix of per-request span counts
+  uint32_t* counters;  // [1]: next dynamic chunk to claim (zero between dispatches)
   int64_t num_blocks;
   int32_t bs;
   int32_t max_blocks_per_seq;
@@ -69,9 +73,17 @@ struct Params {
 };
 
 template <int D>
-struct Span {
-  u32x4 k[2][D / 32];   // K operands of the span's two blocks
-  u32x2 v[2][D / 16];   // V^T operand halves of the two blocks
+struct KOps {
+  u32x4 k[2][D / 32];   // K operands of a span's two blocks
+};
+
+template <int D>
+struct VOps {
+  u32x2 v[2][D / 16];   // V^T operand halves of a span's two blocks
+};
+
+struct SpanRef {
+  int64_t hb0, hb1;     // element offsets of the two blocks' (block, KV head) tiles
   int32_t t;            // first token of the span
   bool bad0, bad1;      // block id out of range
 };
@@ -86,64 +98,89 @@ __device__ inline float wave_sum_groups(float x) {
   return x + __shfl_xor(x, 32);
 }
 
-__device__ inline uint32_t keep_mask(int n_valid_pairs_elems) {
+__device__ inline uint32_t keep_mask(int n_valid_elems) {
   // mask for one 32-bit word holding two bf16 (element 0 in the low half)
-  return n_valid_pairs_elems <= 0 ? 0u : (n_valid_pairs_elems == 1 ? 0x0000ffffu : 0xffffffffu);
+  return n_valid_elems <= 0 ? 0u : (n_valid_elems == 1 ? 0x0000ffffu : 0xffffffffu);
+}
+
+// The span of the request starting at token t (blocks t/16 and t/16 + 1).
+// Block ids are wave-uniform, so they are fetched with scalar loads, which
+// keep the vector-memory counter free for the K/V stream.
+template <int D>
+__device__ inline SpanRef span_ref(const Params& p, const int32_t* __restrict__ bt, int t, int L,
+                                   int g) {
+  SpanRef s;
+  s.t = t;
+  const int b0 = t / kBlock;
+  const bool has1 = t + kBlock < L;
+  int32_t id0 = bt[b0];
+  int32_t id1 = has1 ? bt[b0 + 1] : id0;
+  s.bad0 = id0 < 0 || id0 >= p.num_blocks;
+  if (s.bad0) id0 = 0;
+  const bool bad1 = id1 < 0 || id1 >= p.num_blocks;
+  s.bad1 = has1 && bad1;
+  if (!has1 || bad1) id1 = id0;
+  s.hb0 = ((int64_t)id0 * p.num_kv_heads + g) * (D * kBlock);
+  s.hb1 = ((int64_t)id1 * p.num_kv_heads + g) * (D * kBlock);
+  return s;
 }
 
 template <int D>
-__device__ inline void issue_span(Span<D>& s, const Params& p, const int32_t* bt, int g,
-                                  int t, int L, int lane) {
+__device__ inline void load_k(KOps<D>& o, const uint16_t* kc, const SpanRef& s, int lane) {
   const int row = lane & 15, grp = lane >> 4;
-  s.t = t;
-  const int b0 = t / kBlock;
-  int32_t id0 = bt[b0];
-  int32_t id1 = (t + kBlock < L) ? bt[b0 + 1] : id0;
-  s.bad0 = id0 < 0 || id0 >= p.num_blocks;
-  if (s.bad0) id0 = 0;
-  s.bad1 = (t + kBlock < L) && (id1 < 0 || id1 >= p.num_blocks);
-  if (id1 < 0 || id1 >= p.num_blocks) id1 = id0;
-  const int64_t hb0 = ((int64_t)id0 * p.num_kv_heads + g) * (D * kBlock);
-  const int64_t hb1 = ((int64_t)id1 * p.num_kv_heads + g) * (D * kBlock);
-  const uint16_t* k0 = p.k_cache + hb0;
-  const uint16_t* k1 = p.k_cache + hb1;
-  const uint16_t* v0 = p.v_cache + hb0;
-  const uint16_t* v1 = p.v_cache + hb1;
+  const uint16_t* k0 = kc + s.hb0;
+  const uint16_t* k1 = kc + s.hb1;
 #pragma unroll
   for (int kk = 0; kk < D / 32; ++kk) {
     const int off = ((kk * 4 + grp) * kBlock + row) * 8;
-    s.k[0][kk] = __builtin_nontemporal_load((const u32x4*)(k0 + off));
-    s.k[1][kk] = __builtin_nontemporal_load((const u32x4*)(k1 + off));
-  }
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    const int off = (dt * 16 + row) * kBlock + grp * 4;
-    s.v[0][dt] = __builtin_nontemporal_load((const u32x2*)(v0 + off));
-    s.v[1][dt] = __builtin_nontemporal_load((const u32x2*)(v1 + off));
+    o.k[0][kk] = __builtin_nontemporal_load((const u32x4*)(k0 + off));
+    o.k[1][kk] = __builtin_nontemporal_load((const u32x4*)(k1 + off));
   }
 }
 
+template <int D>
+__device__ inline void load_v(VOps<D>& o, const uint16_t* vc, const SpanRef& s, int lane) {
+  const int row = lane & 15, grp = lane >> 4;
+  const uint16_t* v0 = vc + s.hb0;
+  const uint16_t* v1 = vc + s.hb1;
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    const int off = (dt * 16 + row) * kBlock + grp * 4;
+    o.v[0][dt] = __builtin_nontemporal_load((const u32x2*)(v0 + off));
+    o.v[1][dt] = __builtin_nontemporal_load((const u32x2*)(v1 + off));
+  }
+}
+
+// S^T[token][row] of the span's two blocks.  Q operands come from this
+// wave's LDS copy, stored in operand order: one 16-byte run per lane per
+// (row tile, k-step), so every read is conflict-free.
 template <int D, int MT>
-__device__ inline void compute_span(const Span<D>& s, const bf16x8 (&qop)[MT][D / 32],
-                                    f32x4 (&acc)[MT][D / 16], float (&m_run)[MT],
-                                    float (&l_run)[MT], const int (&pos)[MT], int L,
-                                    int win, float scale_log2, int lane) {
-  const int grp = lane >> 4;
-  // scores S^T[token][row] for both blocks
-  f32x4 st[2][MT];
+__device__ inline void span_scores(const KOps<D>& k, const u32x4* qlds, int lane,
+                                   f32x4 (&st)[2][MT]) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int mt = 0; mt < MT; ++mt) {
+    f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      f32x4 c = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < D / 32; ++kk)
-        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, s.k[h][kk]),
-                                                    qop[mt][kk], c, 0, 0, 0);
-      st[h][mt] = c;
+    for (int kk = 0; kk < D / 32; ++kk) {
+      const bf16x8 qo = __builtin_bit_cast(bf16x8, qlds[(mt * (D / 32) + kk) * 64 + lane]);
+      c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, k.k[0][kk]), qo,
+                                                   c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, k.k[1][kk]), qo,
+                                                   c1, 0, 0, 0);
     }
+    st[0][mt] = c0;
+    st[1][mt] = c1;
+  }
+}
+
+// Online-softmax update from one span's scores; returns P^T operands (bf16).
+template <int D, int MT>
+__device__ inline void span_softmax(const f32x4 (&st)[2][MT], const SpanRef& s,
+                                    f32x4 (&acc)[MT][D / 16], float (&m_run)[MT],
+                                    float (&l_run)[MT], const int (&pos)[MT], int win,
+                                    float scale_log2, int lane, bf16x8 (&pop)[MT]) {
+  const int grp = lane >> 4;
   const bool need_mask = (s.t + kSpan > win) || s.bad0 || s.bad1;
-  bf16x8 pop[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     float x[2][4];
@@ -188,7 +225,13 @@ __device__ inline void compute_span(const Span<D>& s, const bf16x8 (&qop)[MT][D 
     pop[mt] = bf16x8{(__bf16)pr[0][0], (__bf16)pr[0][1], (__bf16)pr[0][2], (__bf16)pr[0][3],
                      (__bf16)pr[1][0], (__bf16)pr[1][1], (__bf16)pr[1][2], (__bf16)pr[1][3]};
   }
-  // V^T operands; elements of tokens >= L (or of bad blocks) are zeroed
+}
+
+// O^T += V^T P^T; V elements of tokens >= L (or of bad blocks) are zeroed.
+template <int D, int MT>
+__device__ inline void span_pv(const VOps<D>& v, const SpanRef& s, int L,
+                               const bf16x8 (&pop)[MT], f32x4 (&acc)[MT][D / 16], int lane) {
+  const int grp = lane >> 4;
   uint32_t keep[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
   if (s.t + kSpan > L || s.bad0 || s.bad1) {
 #pragma unroll
@@ -201,8 +244,8 @@ __device__ inline void compute_span(const Span<D>& s, const bf16x8 (&qop)[MT][D 
   }
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) {
-    const u32x4 w = {s.v[0][dt].x & keep[0], s.v[0][dt].y & keep[1], s.v[1][dt].x & keep[2],
-                     s.v[1][dt].y & keep[3]};
+    const u32x4 w = {v.v[0][dt].x & keep[0], v.v[0][dt].y & keep[1], v.v[1][dt].x & keep[2],
+                     v.v[1][dt].y & keep[3]};
     const bf16x8 vop = __builtin_bit_cast(bf16x8, w);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -210,14 +253,24 @@ __device__ inline void compute_span(const Span<D>& s, const bf16x8 (&qop)[MT][D 
   }
 }
 
-__device__ inline int clamp_len(const Params& p, int r) {
-  const int L = p.seq_lens[r];
+__device__ inline int clamp_len(const Params& p, const int32_t* __restrict__ seq_lens, int r) {
+  const int L = seq_lens[r];
   return max(0, min(L, min(p.max_seq_len, p.max_blocks_per_seq * kBlock)));
 }
 
 // Spans of one (request, KV head) item; an empty context still owns one span
 // so that its rows are written (as zeros).
 __device__ inline int spans_of(int L) { return max(1, (L + kSpan - 1) / kSpan); }
+
+// Values every lane of a wave agrees on, marked so for the compiler (uniform
+// values live in scalar registers and their loads become scalar loads).
+__device__ inline int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ inline int64_t uniform64(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 
 __device__ inline int64_t wave_sum_i64(int64_t x) {
 #pragma unroll
@@ -234,92 +287,79 @@ __device__ inline int64_t wave_incl_scan_i64(int64_t x, int lane) {
   return x;
 }
 
-// First span of wave w's range of the T global spans split over W waves.
-__device__ inline int64_t range_start(int64_t w, int64_t total, int64_t waves) {
-  return w * total / waves;
+constexpr int kStaticPct = 100;  // share of spans split evenly over the waves up front
+constexpr int kChunkSpans = 8;   // spans per dynamically claimed chunk
+
+// The global sequence of T spans (ordered by request, then KV head, then
+// position) is cut into ranges: W static ranges covering the first Ts spans
+// evenly, one per wave, then C dynamic chunks of kChunkSpans spans that waves
+// claim from a counter once their static range is done.  Waves on slower
+// paths to memory (the XCDs differ) thereby end together.  Every kernel
+// derives the same ranges from T and W.
+struct Ranges {
+  int64_t T, Ts, W, C;
+  __device__ Ranges(int64_t total, int64_t waves) : T(total), W(waves) {
+    Ts = total * kStaticPct / 100;
+    C = (total - Ts + kChunkSpans - 1) / kChunkSpans;
+  }
+  __device__ int64_t begin(int64_t rid) const {
+    return rid < W ? rid * Ts / W : Ts + (rid - W) * kChunkSpans;
+  }
+  __device__ int64_t end(int64_t rid) const {
+    return rid < W ? (rid + 1) * Ts / W : min(T, Ts + (rid - W + 1) * kChunkSpans);
+  }
+  // range holding span s
+  __device__ int64_t of(int64_t s) const {
+    return s < Ts ? ((s + 1) * W - 1) / Ts : W + (s - Ts) / kChunkSpans;
+  }
+};
+
+// Request whose spans [hkv*pre[r], hkv*pre[r+1]) contain global span s.
+__device__ inline int find_request(const uint32_t* pre, int bs, int hkv, int64_t s) {
+  int lo = 0, hi = bs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((int64_t)hkv * pre[mid] <= s) lo = mid; else hi = mid - 1;
+  }
+  return lo;
 }
 
-// The wave whose range holds global span s.
-__device__ inline int64_t wave_of(int64_t s, int64_t total, int64_t waves) {
-  return ((s + 1) * waves - 1) / total;
+// One span: S from K, online softmax, PV from V; with LOADS the registers
+// each phase has consumed are refilled at once with the span `nr`.
+template <int D, int MT, bool LOADS>
+__device__ inline void span_step(KOps<D>& kr, VOps<D>& vr, const SpanRef& sr, const SpanRef& nr,
+                                 const u32x4* qlds, const Params& p, f32x4 (&acc)[MT][D / 16],
+                                 float (&m_run)[MT], float (&l_run)[MT], const int (&pos)[MT],
+                                 int win, int L, int lane) {
+  f32x4 st[2][MT];
+  span_scores<D, MT>(kr, qlds, lane, st);
+  if constexpr (LOADS) load_k<D>(kr, p.k_cache, nr, lane);
+  bf16x8 pop[MT];
+  span_softmax<D, MT>(st, sr, acc, m_run, l_run, pos, win, p.scale_log2, lane, pop);
+  span_pv<D, MT>(vr, sr, L, pop, acc, lane);
+  if constexpr (LOADS) load_v<D>(vr, p.v_cache, nr, lane);
 }
 
-// Stream-K decomposition: the global sequence of spans, ordered by request,
-// then KV head, then position, is cut into W equal contiguous ranges, one per
-// resident wave.  A wave runs the online softmax over every (request, KV head)
-// item its range touches; an item wholly inside the range is finished and
-// written directly, an item cut by a range boundary leaves a partial (running
-// max, sum, unnormalised O) in the wave's head slot (item began in an earlier
-// range) or tail slot (item continues in a later range) for the merge kernel.
-template <int D, int MT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT <= 2 ? 2 : 1)))
-void verify_attention_kernel(Params p) {
-  __shared__ int64_t s_wsum[4];
-  __shared__ int s_r0[4];
-  __shared__ int64_t s_p0[4];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+// One range [s, s1) of global spans, range id rid: online softmax over every
+// (request, KV head) item the range touches.  An item wholly inside the range
+// is finished and written; an item cut by a range boundary leaves a partial
+// (running max, sum, unnormalised O) in the range's head slot (the item began
+// in an earlier range) or tail slot (it continues in a later one).
+template <int D, int MT, int DEPTH>
+__device__ void process_range(const Params& p, const int32_t* __restrict__ block_table,
+                              const int32_t* __restrict__ seq_lens,
+                              const int32_t* __restrict__ q_indptr, const uint32_t* pre,
+                              u32x4* qlds, int64_t rid, int64_t s, int64_t s1, int lane) {
   const int grp = lane >> 4;
-  const int64_t W = p.num_waves;
   const int hkv = p.num_kv_heads;
-
-  // total spans T
-  int64_t local = 0;
-  for (int r = tid; r < p.bs; r += 256) local += spans_of(clamp_len(p, r));
-  local = wave_sum_i64(local);
-  if (lane == 0) s_wsum[wave] = local;
-  if (tid < 4) s_r0[tid] = -1;
-  __syncthreads();
-  const int64_t T = (s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3]) * hkv;
-  int64_t ws0[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t w = (int64_t)blockIdx.x * 4 + i;
-    ws0[i] = range_start(w, T, W);
-    if (tid == 0 && (w >= W || ws0[i] >= range_start(w + 1, T, W))) s_r0[i] = -2;  // empty
-  }
-  // exclusive prefix of per-request span counts; locate each wave's first request
-  int64_t carry = 0;
-  for (int base = 0; base < p.bs; base += 256) {
-    const int r = base + tid;
-    const int64_t n = r < p.bs ? spans_of(clamp_len(p, r)) : 0;
-    const int64_t incl = wave_incl_scan_i64(n, lane);
-    __syncthreads();
-    if (lane == 63) s_wsum[wave] = incl;
-    __syncthreads();
-    int64_t before = carry;
-    for (int i = 0; i < wave; ++i) before += s_wsum[i];
-    const int64_t excl = before + incl - n;
-    if (r < p.bs) {
-      if (blockIdx.x == 0) p.prefix[r] = excl;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (hkv * excl <= ws0[i] && ws0[i] < hkv * (excl + n)) {
-          s_r0[i] = r;
-          s_p0[i] = excl;
-        }
-    }
-    carry += s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
-    __syncthreads();
-    const bool found = s_r0[0] != -1 && s_r0[1] != -1 && s_r0[2] != -1 && s_r0[3] != -1;
-    if (blockIdx.x != 0 && found) break;
-  }
-  if (blockIdx.x == 0 && tid == 0) p.prefix[p.bs] = carry;
-  __syncthreads();
-
-  const int64_t w = (int64_t)blockIdx.x * 4 + wave;
-  int r = s_r0[wave];
-  if (r < 0) return;
-  int64_t pr = s_p0[wave];
-  int64_t s = ws0[wave];
-  const int64_t s1 = range_start(w + 1, T, W);
-
+  int r = uniform(find_request(pre, p.bs, hkv, s));
+  int64_t pr = pre[r];
   while (s < s1) {
-    const int L = clamp_len(p, r);
+    __builtin_amdgcn_wave_barrier();
+    const int L = clamp_len(p, seq_lens, r);
     const int n = spans_of(L);
-    const int qo = p.q_indptr[r];
-    const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
+    const int qo = q_indptr[r];
+    const int nq = max(0, min(q_indptr[r + 1] - qo, p.max_q));
     const int64_t off = s - hkv * pr;
     const int g = (int)(off / n);
     const int j0 = (int)(off - (int64_t)g * n);
@@ -327,7 +367,6 @@ void verify_attention_kernel(Params p) {
     const int rows = p.group * nq;
     const int win = L - nq;
 
-    bf16x8 qop[MT][D / 32];
     int pos[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -338,14 +377,16 @@ void verify_attention_kernel(Params p) {
         const uint16_t* src = p.q + ((int64_t)(qo + j) * p.num_q_heads + h) * D;
 #pragma unroll
         for (int kk = 0; kk < D / 32; ++kk)
-          qop[mt][kk] = __builtin_bit_cast(bf16x8, *(const u32x4*)(src + kk * 32 + grp * 8));
+          qlds[(mt * (D / 32) + kk) * 64 + lane] = *(const u32x4*)(src + kk * 32 + grp * 8);
         pos[mt] = win + j;
       } else {
 #pragma unroll
-        for (int kk = 0; kk < D / 32; ++kk) qop[mt][kk] = bf16x8{};
+        for (int kk = 0; kk < D / 32; ++kk)
+          qlds[(mt * (D / 32) + kk) * 64 + lane] = u32x4{0, 0, 0, 0};
         pos[mt] = L - 1;
       }
     }
+    __builtin_amdgcn_wave_barrier();
     f32x4 acc[MT][D / 16];
     float m_run[MT], l_run[MT];
 #pragma unroll
@@ -355,12 +396,63 @@ void verify_attention_kernel(Params p) {
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) acc[mt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const int32_t* bt = p.block_table + (int64_t)r * p.max_blocks_per_seq;
-    for (int j = j0; j < j1; ++j) {
-      Span<D> sp;
-      issue_span<D>(sp, p, bt, g, j * kSpan, L, lane);
-      compute_span<D, MT>(sp, qop, acc, m_run, l_run, pos, L, win, p.scale_log2, lane);
+
+    // Software pipeline over spans.  With DEPTH = 1, K(j+1) is requested as
+    // soon as S(j) has consumed K(j) and V(j+1) as soon as PV(j) has consumed
+    // V(j); with DEPTH = 2 (when registers allow only one wave per SIMD anyway)
+    // two buffers alternate and spans j+1 and j+2 are in flight during span j.
+    // Loads inside the loops are unconditional (tails are peeled): a
+    // conditional load would force a full drain of the load counter per span.
+    const int32_t* __restrict__ bt = block_table + (int64_t)r * p.max_blocks_per_seq;
+#define NSD_STEP(LOADS, KR, VR, SR, NR)                                                         \
+  span_step<D, MT, LOADS>(KR, VR, SR, NR, qlds, p, acc, m_run, l_run, pos, win, L, lane)
+    if constexpr (DEPTH == 1) {
+      SpanRef cur = span_ref<D>(p, bt, j0 * kSpan, L, g);
+      KOps<D> kreg;
+      VOps<D> vreg;
+      load_k<D>(kreg, p.k_cache, cur, lane);
+      load_v<D>(vreg, p.v_cache, cur, lane);
+      for (int j = j0; j + 1 < j1; ++j) {
+        const SpanRef nxt = span_ref<D>(p, bt, (j + 1) * kSpan, L, g);
+        NSD_STEP(true, kreg, vreg, cur, nxt);
+        cur = nxt;
+      }
+      NSD_STEP(false, kreg, vreg, cur, cur);
+    } else {
+      SpanRef ra = span_ref<D>(p, bt, j0 * kSpan, L, g);
+      SpanRef rb = ra;
+      KOps<D> ka, kb;
+      VOps<D> va, vb;
+      load_k<D>(ka, p.k_cache, ra, lane);
+      load_v<D>(va, p.v_cache, ra, lane);
+      if (j0 + 1 < j1) {
+        rb = span_ref<D>(p, bt, (j0 + 1) * kSpan, L, g);
+        load_k<D>(kb, p.k_cache, rb, lane);
+        load_v<D>(vb, p.v_cache, rb, lane);
+      }
+      int j = j0;
+      for (; j + 3 < j1; j += 2) {
+        const SpanRef na = span_ref<D>(p, bt, (j + 2) * kSpan, L, g);
+        NSD_STEP(true, ka, va, ra, na);
+        const SpanRef nb = span_ref<D>(p, bt, (j + 3) * kSpan, L, g);
+        NSD_STEP(true, kb, vb, rb, nb);
+        ra = na;
+        rb = nb;
+      }
+      const int rem = j1 - j;
+      if (rem == 3) {
+        const SpanRef na = span_ref<D>(p, bt, (j + 2) * kSpan, L, g);
+        NSD_STEP(true, ka, va, ra, na);
+        NSD_STEP(false, kb, vb, rb, rb);
+        NSD_STEP(false, ka, va, na, na);
+      } else if (rem == 2) {
+        NSD_STEP(false, ka, va, ra, ra);
+        NSD_STEP(false, kb, vb, rb, rb);
+      } else {
+        NSD_STEP(false, ka, va, ra, ra);
+      }
     }
+#undef NSD_STEP
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) l_run[mt] = wave_sum_groups(l_run[mt]);
 
@@ -382,7 +474,7 @@ void verify_attention_kernel(Params p) {
         }
       }
     } else {
-      const int64_t slot = 2 * w + (j0 > 0 ? 0 : 1);
+      const int64_t slot = 2 * rid + (j0 > 0 ? 0 : 1);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = mt * 16 + (lane & 15);
@@ -401,39 +493,99 @@ void verify_attention_kernel(Params p) {
   }
 }
 
-// Merge the partials of every item that a range boundary cut, in wave order
+// One dispatch of W waves (W / 4 workgroups of 4 independent waves).
+template <int D, int MT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D * MT <= 128 ? 2 : 1)))
+void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
+                             const int32_t* __restrict__ seq_lens,
+                             const int32_t* __restrict__ q_indptr) {
+  extern __shared__ uint32_t s_pre[];        // [bs + 1]: exclusive prefix of per-request spans
+  __shared__ uint32_t s_wsum[4];
+  __shared__ u32x4 s_q[4][MT * (D / 32) * 64];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = uniform(tid >> 6);
+
+  // prefix of per-request span counts (every workgroup keeps its own copy)
+  uint32_t carry = 0;
+  for (int base = 0; base < p.bs; base += 256) {
+    const int r = base + tid;
+    const uint32_t n = r < p.bs ? spans_of(clamp_len(p, seq_lens, r)) : 0;
+    uint32_t incl = n;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    uint32_t before = carry;
+    for (int i = 0; i < wave; ++i) before += s_wsum[i];
+    if (r < p.bs) {
+      s_pre[r] = before + incl - n;
+      if (blockIdx.x == 0) p.prefix[r] = before + incl - n;
+    }
+    carry += s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    s_pre[p.bs] = carry;
+    if (blockIdx.x == 0) p.prefix[p.bs] = carry;
+  }
+  __syncthreads();
+
+  const Ranges R((int64_t)p.num_kv_heads * carry, p.num_waves);
+  const int64_t w = (int64_t)blockIdx.x * 4 + wave;
+  u32x4* qlds = s_q[wave];
+  int64_t rid = w;
+  while (true) {
+    const int64_t b = uniform64(R.begin(rid)), e = uniform64(R.end(rid));
+    if (b < e)
+      process_range<D, MT, 1>(p, block_table, seq_lens, q_indptr, s_pre,
+                                                     qlds, rid, b, e, lane);
+    uint32_t c = 0;
+    if (lane == 0)
+      c = __hip_atomic_fetch_add(p.counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    c = uniform(__shfl(c, 0));
+    if (c >= R.C) break;
+    rid = R.W + c;
+  }
+}
+
+// Merge the partials of every item that a range boundary cut, in range order
 // (deterministic, no atomics).
 template <int D, int MT>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const int g = blockIdx.x;
   const int r = blockIdx.y;
+  // the attention dispatch has finished: rewind its chunk counter for the next one
+  if (g == 0 && r == 0 && threadIdx.x == 0) *p.counters = 0;
   const int hkv = p.num_kv_heads;
-  const int64_t W = p.num_waves;
-  const int64_t T = p.prefix[p.bs] * hkv;
-  const int L = clamp_len(p, r);
+  const Ranges R((int64_t)hkv * p.prefix[p.bs], p.num_waves);
+  const int L = clamp_len(p, p.seq_lens, r);
   const int n = spans_of(L);
   const int qo = p.q_indptr[r];
   const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
-  const int64_t a = p.prefix[r] * hkv + (int64_t)g * n;
-  const int64_t wa = wave_of(a, T, W);
-  const int64_t wb = wave_of(a + n - 1, T, W);
-  if (wa == wb || nq == 0) return;
+  const int64_t a = (int64_t)p.prefix[r] * hkv + (int64_t)g * n;
+  const int64_t ra = R.of(a);
+  const int64_t rb = R.of(a + n - 1);
+  if (ra == rb || nq == 0) return;
   const int rows = p.group * nq;
   constexpr int kVec = D / 4;
   for (int idx = threadIdx.x; idx < rows * kVec; idx += blockDim.x) {
     const int m = idx / kVec;
     const int d = (idx % kVec) * 4;
     float mx = -INFINITY;
-    for (int64_t w = wa; w <= wb; ++w) {
-      if (w > wa && range_start(w, T, W) == range_start(w + 1, T, W)) continue;
-      const int64_t slot = 2 * w + (w == wa ? 1 : 0);
+    for (int64_t q = ra; q <= rb; ++q) {
+      if (R.begin(q) >= R.end(q)) continue;
+      const int64_t slot = 2 * q + (q == ra ? 1 : 0);
       mx = fmaxf(mx, p.part_ml[slot * (MT * 16) + m].x);
     }
     f32x4 num = {0.f, 0.f, 0.f, 0.f};
     float den = 0.f;
-    for (int64_t w = wa; w <= wb; ++w) {
-      if (w > wa && range_start(w, T, W) == range_start(w + 1, T, W)) continue;
-      const int64_t slot = 2 * w + (w == wa ? 1 : 0);
+    for (int64_t q = ra; q <= rb; ++q) {
+      if (R.begin(q) >= R.end(q)) continue;
+      const int64_t slot = 2 * q + (q == ra ? 1 : 0);
       const float2 ml = p.part_ml[slot * (MT * 16) + m];
       const float wt = (ml.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml.x - mx);
       const f32x4 o = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
@@ -475,7 +627,9 @@ const void* kernel_for(int d, int mt) {
 struct Plan {
   int mt;            // 16-row tiles
   int num_waves;     // W: resident waves of the launch
-  size_t prefix_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
+  int64_t max_chunks;
+  size_t lds_bytes;  // dynamic LDS: the span prefix
+  size_t counter_bytes, prefix_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
 };
 
 // Waves the device keeps resident for this kernel (CUs x waves per CU), or
@@ -500,25 +654,31 @@ int resident_waves(int d, int mt) {
 }
 
 bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, Plan* pl) {
-  if (bs < 0 || hq < 1 || hkv < 1 || hq % hkv || (d != 64 && d != 128) || max_q < 1 ||
-      max_seq_len < 0)
+  if (bs < 0 || bs > kMaxBatch || hq < 1 || hkv < 1 || hq % hkv || (d != 64 && d != 128) ||
+      max_q < 1 || max_seq_len < 0)
     return false;
   const int rows = (hq / hkv) * max_q;
   if (rows > kMaxRows) return false;
   pl->mt = (rows + 15) / 16;
   pl->num_waves = resident_waves(d, pl->mt);
-  const size_t slots = 2 * (size_t)pl->num_waves * pl->mt * 16;
-  pl->prefix_bytes = (((size_t)bs + 1) * sizeof(int64_t) + 255) / 256 * 256;
+  // upper bound of the dynamic chunks: at most 1 + (100-kStaticPct)% of the spans
+  const int64_t max_spans = (int64_t)hkv * bs * std::max(1, (max_seq_len + kSpan - 1) / kSpan);
+  pl->max_chunks = (max_spans - max_spans * kStaticPct / 100 + kChunkSpans - 1) / kChunkSpans + 1;
+  const size_t slots = 2 * ((size_t)pl->num_waves + (size_t)pl->max_chunks) * pl->mt * 16;
+  pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t);
+  pl->counter_bytes = 256;
+  pl->prefix_bytes = (((size_t)bs + 1) * sizeof(uint32_t) + 255) / 256 * 256;
   pl->part_o_bytes = slots * d * sizeof(float);
   pl->part_ml_bytes = slots * sizeof(float2);
-  pl->ws_bytes = pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes;
+  pl->ws_bytes = pl->counter_bytes + pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes;
   return true;
 }
 
 template <int D, int MT>
 void launch(const Params& p, int bs, hipStream_t stream) {
-  hipLaunchKernelGGL((verify_attention_kernel<D, MT>), dim3(p.num_waves / 4), dim3(256), 0,
-                     stream, p);
+  hipLaunchKernelGGL((verify_attention_kernel<D, MT>), dim3(p.num_waves / 4), dim3(256),
+                     ((size_t)bs + 1) * sizeof(uint32_t), stream, p, p.block_table, p.seq_lens,
+                     p.q_indptr);
   hipLaunchKernelGGL((combine_kernel<D, MT>), dim3(p.num_kv_heads, bs), dim3(256), 0, stream, p);
 }
 
@@ -555,7 +715,8 @@ extern "C" nsd_status nsd_verify_attention(const void* q, const void* k_cache,
                                            float scale, void* out, void* workspace,
                                            size_t workspace_bytes, void* stream) {
   using namespace nsd;
-  if (bs < 0 || bs > 65535) return fail(NSD_ERR_SHAPE, "verify_attention: bs must be in [0, 65535]");
+  if (bs < 0 || bs > kMaxBatch)
+    return fail(NSD_ERR_SHAPE, "verify_attention: bs must be in [0, %d]", kMaxBatch);
   if (block_size != NSD_BLOCK_SIZE)
     return fail(NSD_ERR_UNSUPPORTED, "verify_attention: block_size must be 16 (got %d)", block_size);
   if (head_dim != 64 && head_dim != 128)
@@ -582,6 +743,17 @@ extern "C" nsd_status nsd_verify_attention(const void* q, const void* k_cache,
     return fail(NSD_ERR_WORKSPACE, "verify_attention: workspace of %zu bytes needed, %zu given",
                 pl.ws_bytes, workspace ? workspace_bytes : (size_t)0);
 
+  int dev = 0, lds_max = 0;
+  hipFuncAttributes fa;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
+          hipSuccess &&
+      hipFuncGetAttributes(&fa, kernel_for(head_dim, pl.mt)) == hipSuccess &&
+      fa.sharedSizeBytes + pl.lds_bytes > (size_t)lds_max)
+    return fail(NSD_ERR_UNSUPPORTED, "verify_attention: bs=%d needs %zu bytes of LDS, %d available",
+                bs, fa.sharedSizeBytes + pl.lds_bytes, lds_max);
+  (void)hipGetLastError();
+
   Params p;
   p.q = (const uint16_t*)q;
   p.k_cache = (const uint16_t*)k_cache;
@@ -590,9 +762,10 @@ extern "C" nsd_status nsd_verify_attention(const void* q, const void* k_cache,
   p.seq_lens = seq_lens;
   p.q_indptr = q_indptr;
   p.out = (uint16_t*)out;
-  p.prefix = (int64_t*)workspace;
-  p.part_o = (float*)((char*)workspace + pl.prefix_bytes);
-  p.part_ml = (float2*)((char*)workspace + pl.prefix_bytes + pl.part_o_bytes);
+  p.counters = (uint32_t*)workspace;
+  p.prefix = (uint32_t*)((char*)workspace + pl.counter_bytes);
+  p.part_o = (float*)((char*)workspace + pl.counter_bytes + pl.prefix_bytes);
+  p.part_ml = (float2*)((char*)workspace + pl.counter_bytes + pl.prefix_bytes + pl.part_o_bytes);
   p.num_blocks = num_blocks;
   p.bs = bs;
   p.max_blocks_per_seq = max_blocks_per_seq;
