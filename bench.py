@@ -29,7 +29,38 @@ def parse():
     ap.add_argument("--workload", default="verify_8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy three times (counter calibration)")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "verify_attention_traffic.json")
+
+
+def measured_traffic(kernel_src):
+    """HBM bytes per verify_attention call from the committed counter runs, or None
+    when the kernel source has changed since those counters were taken."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+        digest = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_sha256") != digest:
+        return None
+    return rec.get("bytes_per_call")
+
+
+def calibrate_copy():
+    import torch
+    n = 1 << 30
+    a = torch.ones(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n,
+                      "dispatches": 3}), flush=True)
 
 
 def describe(cfg):
@@ -110,6 +141,9 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; use --gpus 1"}))
         sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     import torch
     import paper_2609_29364_amd as nsd
     from workload import CONFIGS, make_meta, make_layer, make_accept
@@ -186,7 +220,9 @@ def main():
         "gather_attention_tbs": round((gb + ab) / ((g_ms + a_ms) * 1e-3) / 1e12, 3),
         "roofline": {"bound": "hbm", "kernel": "verify_attention", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(os.path.join(
+                         ROOT, "paper_2609_29364_amd", "csrc", "verify_attention.hip")),
                      "alg_bytes_per_launch": ab},
         "wall_s_timed": round(t_wall, 3),
     }
