@@ -9,6 +9,9 @@
  *                         queries of every request over the paged KV cache
  *   nsd_spec_accept       acceptance of proposals and residual resampling
  *
+ * nsd_gather_verify_attention does the first two in one pass (each staged
+ * byte read once).
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Pointers named as device pointers must address memory the GPU of
@@ -99,7 +102,8 @@ nsd_status nsd_kv_gather(const void* src_k, const void* src_v, int64_t src_num_b
                          void* stream);
 
 /*
- * Bytes of workspace nsd_verify_attention needs for these sizes on the
+ * Bytes of workspace nsd_verify_attention and nsd_gather_verify_attention
+ * need for these sizes on the
  * current HIP device (0 if the sizes are invalid).  The size depends on the
  * arguments and on how many waves the device keeps resident (its CU count);
  * the environment variable NSD_ATTN_WAVES (a positive multiple of 4), if set,
@@ -152,6 +156,40 @@ nsd_status nsd_verify_attention(const void* q, const void* k_cache, const void* 
                                 int32_t max_q_per_seq, int32_t max_seq_len, float scale,
                                 void* out, void* workspace, size_t workspace_bytes,
                                 void* stream);
+
+/*
+ * KV-state preparation fused with verification attention, for one layer.
+ *
+ * Passage: Algorithm 1 (Prepare makes an arriving request's KV state resident
+ * on the worker, then Run verifies); Appendix E.1 (the state comes from a
+ * stable per-request extent of blocks).  Same computation and arguments as
+ * nsd_verify_attention, plus:
+ *   k_stage, v_stage : device, staging planes of this layer, bf16
+ *                      [stage_num_blocks][...] (layout above);
+ *   stage_table      : device, int32 [bs][max_blocks_per_seq]; row r holds the
+ *                      staging block of each of request r's blocks if r is
+ *                      arriving (entry 0 >= 0), or -1 in entry 0 if r is
+ *                      resident in the worker pool.
+ * For an arriving request, block b (b < ceil(L_r/16)) is read from
+ * k/v_stage[stage_table[r][b]] instead of the worker pool, and the whole block
+ * (all KV heads, all 16 slots) is written to k/v_cache[block_table[r][b]], as
+ * nsd_kv_gather with the pairs (stage_table[r][b], block_table[r][b]) would:
+ * each staged byte is read from HBM once.  The caches are therefore read and
+ * written (non-const); the blocks of different requests must be distinct.
+ * stage_num_blocks == 0 treats every request as resident.  Staging ids
+ * outside [0, stage_num_blocks) make their tokens invisible; destination ids
+ * outside [0, num_blocks) are not written.
+ */
+nsd_status nsd_gather_verify_attention(const void* q, void* k_cache, void* v_cache,
+                                       int64_t num_blocks, const void* k_stage,
+                                       const void* v_stage, int64_t stage_num_blocks,
+                                       const int32_t* block_table, const int32_t* stage_table,
+                                       int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                       const int32_t* q_indptr, int32_t bs, int32_t num_q_heads,
+                                       int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                                       int32_t max_q_per_seq, int32_t max_seq_len, float scale,
+                                       void* out, void* workspace, size_t workspace_bytes,
+                                       void* stream);
 
 /*
  * Speculative acceptance with residual resampling.

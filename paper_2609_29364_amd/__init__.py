@@ -37,6 +37,9 @@ _SIGS = {
     "nsd_verify_attention_workspace_size": (_SZ, [_I32, _I32, _I32, _I32, _I32, _I32]),
     "nsd_verify_attention": (_I32, [_P, _P, _P, _I64, _P, _I32, _P, _P, _I32, _I32, _I32, _I32,
                                     _I32, _I32, _I32, _F32, _P, _P, _SZ, _P]),
+    "nsd_gather_verify_attention": (_I32, [_P, _P, _P, _I64, _P, _P, _I64, _P, _P, _I32, _P, _P,
+                                           _I32, _I32, _I32, _I32, _I32, _I32, _I32, _F32, _P,
+                                           _P, _SZ, _P]),
     "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
 }
 
@@ -162,6 +165,50 @@ def verify_attention(q, k_cache, v_cache, block_table, seq_lens, q_indptr, max_q
     return out
 
 
+def gather_verify_attention(q, k_cache, v_cache, k_stage, v_stage, block_table, stage_table,
+                            seq_lens, q_indptr, max_q_per_seq, max_seq_len, scale=None, out=None,
+                            workspace=None):
+    """KV-state preparation fused with one layer of verification attention.
+
+    Arriving requests (stage_table[r][0] >= 0) read their blocks from the
+    staging planes and leave them in k_cache/v_cache at block_table[r][b];
+    returns out [total_q][Hq][D] bf16.
+    """
+    for t, n in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache"), (k_stage, "k_stage"),
+                 (v_stage, "v_stage")):
+        _dev(t, torch.bfloat16, n)
+    for t, n in ((block_table, "block_table"), (stage_table, "stage_table"),
+                 (seq_lens, "seq_lens"), (q_indptr, "q_indptr")):
+        _dev(t, torch.int32, n)
+    total_q, hq, d = q.shape
+    nb, hkv, dv8, bsz, vec = k_cache.shape
+    if dv8 * vec != d or v_cache.shape != (nb, hkv, d, bsz):
+        raise ValueError("cache shapes do not match q")
+    if k_stage.shape[1:] != k_cache.shape[1:] or v_stage.shape[1:] != v_cache.shape[1:] \
+            or k_stage.shape[0] != v_stage.shape[0]:
+        raise ValueError("staging planes do not match the caches")
+    bs = seq_lens.numel()
+    if block_table.dim() != 2 or block_table.shape[0] != bs or q_indptr.numel() != bs + 1 \
+            or stage_table.shape != block_table.shape:
+        raise ValueError("block_table / stage_table / q_indptr do not match seq_lens")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out is None:
+        out = torch.empty_like(q)
+    elif out.shape != q.shape:
+        raise ValueError("out must have q's shape")
+    need = verify_attention_workspace_size(bs, hq, hkv, d, max_q_per_seq, max_seq_len)
+    if workspace is None and need:
+        workspace = new_workspace(need, q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("gather_verify_attention", lib().nsd_gather_verify_attention(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), nb, _ptr(k_stage), _ptr(v_stage),
+        k_stage.shape[0], _ptr(block_table), _ptr(stage_table), block_table.shape[1],
+        _ptr(seq_lens), _ptr(q_indptr), bs, hq, hkv, d, bsz, max_q_per_seq, max_seq_len,
+        float(scale), _ptr(out), _ptr(workspace), ws_bytes, _stream(q)))
+    return out
+
+
 def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, accepted_len=None,
                 out_tokens=None):
     """Acceptance + residual resampling; returns (accepted_len [bs], out_tokens [total_q]) int32."""
@@ -191,5 +238,5 @@ def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, acce
 
 
 __all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
-           "new_workspace",
+           "new_workspace", "gather_verify_attention",
            "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

@@ -18,7 +18,7 @@ from parity import i32, u16, check_attention, check_accept
 pytestmark = pytest.mark.gpu
 
 
-def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None):
+def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None, fused=False):
     layers = layers or [make_layer(cfg, meta, l, "cpu") for l in range(cfg.num_layers)]
     stack = lambda name: torch.stack([getattr(l, name) for l in layers]).to(dev).contiguous()
     kp, vp, ks, vs, q = (stack(n) for n in ("k_pool", "v_pool", "k_stage", "v_stage", "q"))
@@ -31,10 +31,20 @@ def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None):
     if waves:
         os.environ["NSD_ATTN_WAVES"] = str(waves)
     try:
-        outs, acc, tok = verify_round(kp, vp, ks, vs, i32(meta.src_ids, dev), i32(meta.dst_ids, dev),
-                                      q, i32(meta.block_table, dev), i32(meta.seq_lens, dev),
-                                      i32(meta.q_indptr, dev), meta.max_q, meta.max_seq_len,
-                                      accept=acc_dev)
+        if fused:
+            bt, st = i32(meta.block_table, dev), i32(meta.stage_table, dev)
+            sl, qi = i32(meta.seq_lens, dev), i32(meta.q_indptr, dev)
+            outs = [nsd.gather_verify_attention(q[l], kp[l], vp[l], ks[l], vs[l], bt, st, sl, qi,
+                                                meta.max_q, meta.max_seq_len)
+                    for l in range(cfg.num_layers)]
+            acc = tok = None
+            if acc_dev is not None:
+                acc, tok = nsd.spec_accept(*acc_dev[:4], qi, acc_dev[4])
+        else:
+            outs, acc, tok = verify_round(kp, vp, ks, vs, i32(meta.src_ids, dev),
+                                          i32(meta.dst_ids, dev), q, i32(meta.block_table, dev),
+                                          i32(meta.seq_lens, dev), i32(meta.q_indptr, dev),
+                                          meta.max_q, meta.max_seq_len, accept=acc_dev)
         torch.cuda.synchronize()
     finally:
         if waves:
@@ -61,14 +71,16 @@ def _check_all(cfg, meta, dev, **kw):
     return outs
 
 
-def test_tiny_round(device):
+@pytest.mark.parametrize("fused", [False, True])
+def test_tiny_round(device, fused):
     cfg = CONFIGS["tiny"]
-    _check_all(cfg, make_meta(cfg), device)
+    _check_all(cfg, make_meta(cfg), device, fused=fused)
 
 
-def test_tiny_round_shuffled_staging(device):
+@pytest.mark.parametrize("fused", [False, True])
+def test_tiny_round_shuffled_staging(device, fused):
     cfg = custom_config(staging_order="shuffled", seed=10)
-    _check_all(cfg, make_meta(cfg), device)
+    _check_all(cfg, make_meta(cfg), device, fused=fused)
 
 
 CASES = [
@@ -84,14 +96,15 @@ CASES = [
 
 @pytest.mark.parametrize("case", range(len(CASES)))
 @pytest.mark.parametrize("waves", [None, 4, 12])
-def test_attention_edge_cases(device, case, waves):
+@pytest.mark.parametrize("fused", [False, True])
+def test_attention_edge_cases(device, case, waves, fused):
     hq, hkv, d, lens, depth = CASES[case]
     bs = len(lens)
     cfg = custom_config(seed=100 + case, bs=bs, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
                         vocab=0, n_arriving=bs // 2, pool_blocks=None)
     arriving = np.arange(bs) % 2 == 1
     meta = make_meta(cfg, seq_lens=lens, depth=depth, arriving=arriving)
-    _check_all(cfg, meta, device, waves=waves)
+    _check_all(cfg, meta, device, waves=waves, fused=fused)
 
 
 def test_ragged_batch_of_64(device):
@@ -101,9 +114,10 @@ def test_ragged_batch_of_64(device):
     cfg = custom_config(seed=7, bs=64, num_q_heads=32, num_kv_heads=8, head_dim=128, vocab=2048,
                         n_arriving=20, pool_blocks=None, k_lo=0, k_hi=8)
     meta = make_meta(cfg, seq_lens=lens, depth=depth)
-    _check_all(cfg, meta, device)
-    _check_all(cfg, meta, device, waves=8)
-    _check_all(cfg, meta, device, waves=36)
+    for fused in (False, True):
+        _check_all(cfg, meta, device, fused=fused)
+        _check_all(cfg, meta, device, waves=8, fused=fused)
+        _check_all(cfg, meta, device, waves=36, fused=fused)
 
 
 def test_multi_layer_gather_subrange(device):

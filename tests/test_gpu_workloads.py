@@ -63,23 +63,34 @@ def _gather_check(meta, lay, kp, vp, full, seed=0):
     assert np.array_equal(u16(vp[idx]).cpu().numpy(), ref_v[0])
 
 
-def _round(name, device, full_gather):
+def _attend(meta, lay, device, fused):
+    """Gather + attention of one layer, separately or fused; returns (pools, out)."""
+    kp, vp = lay.k_pool.clone(), lay.v_pool.clone()
+    bt, sl, qi = (i32(meta.block_table, device), i32(meta.seq_lens, device),
+                  i32(meta.q_indptr, device))
+    if fused:
+        out = nsd.gather_verify_attention(lay.q, kp, vp, lay.k_stage, lay.v_stage, bt,
+                                          i32(meta.stage_table, device), sl, qi, meta.max_q,
+                                          meta.max_seq_len)
+    else:
+        nsd.kv_gather(lay.k_stage, lay.v_stage, kp, vp, i32(meta.src_ids, device),
+                      i32(meta.dst_ids, device))
+        out = nsd.verify_attention(lay.q, kp, vp, bt, sl, qi, meta.max_q, meta.max_seq_len)
+    return kp, vp, out
+
+
+def _round(name, device, full_gather, fused):
     cfg = CONFIGS[name]
     meta = make_meta(cfg)
     lay = make_layer(cfg, meta, 0, device)
-    kp, vp = lay.k_pool.clone(), lay.v_pool.clone()
-    nsd.kv_gather(lay.k_stage, lay.v_stage, kp, vp, i32(meta.src_ids, device),
-                  i32(meta.dst_ids, device))
-    out = nsd.verify_attention(lay.q, kp, vp, i32(meta.block_table, device),
-                               i32(meta.seq_lens, device), i32(meta.q_indptr, device),
-                               meta.max_q, meta.max_seq_len)
+    kp, vp, out = _attend(meta, lay, device, fused)
     acc_in = make_accept(cfg, meta, device)
     acc = tok = None
     if acc_in is not None:
         acc, tok = nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
                                    acc_in.uniforms, i32(meta.q_indptr, device), cfg.k_hi)
     torch.cuda.synchronize()
-    print(f"{name}: round ran, checking", flush=True)
+    print(f"{name} (fused={fused}): round ran, checking", flush=True)
     _gather_check(meta, lay, kp, vp, full_gather)
     worst = check_attention(meta, lay, out, _sample_requests(meta))
     print(f"{name}: attention max abs error {worst:.3e}", flush=True)
@@ -93,29 +104,27 @@ def _round(name, device, full_gather):
         assert 0.05 < mean_acc < 0.5
 
 
-def test_draft_decode_full(device):
-    _round("draft_decode", device, full_gather=True)
+@pytest.mark.parametrize("fused", [False, True])
+def test_draft_decode_full(device, fused):
+    _round("draft_decode", device, full_gather=True, fused=fused)
 
 
-def test_verify_8b_full(device):
-    _round("verify_8b", device, full_gather=True)
+@pytest.mark.parametrize("fused", [False, True])
+def test_verify_8b_full(device, fused):
+    _round("verify_8b", device, full_gather=True, fused=fused)
 
 
-def test_knee_full(device):
-    _round("knee", device, full_gather=False)
+@pytest.mark.parametrize("fused", [False, True])
+def test_knee_full(device, fused):
+    _round("knee", device, full_gather=False, fused=fused)
 
 
-@pytest.mark.parametrize("layer", [0, 17, 35])
-def test_full_depth_layer(device, layer):
+@pytest.mark.parametrize("layer,fused", [(0, False), (17, True), (35, False), (35, True)])
+def test_full_depth_layer(device, layer, fused):
     cfg = CONFIGS["full_depth"]
     meta = make_meta(cfg)
     lay = make_layer(cfg, meta, layer, device)
-    kp, vp = lay.k_pool.clone(), lay.v_pool.clone()
-    nsd.kv_gather(lay.k_stage, lay.v_stage, kp, vp, i32(meta.src_ids, device),
-                  i32(meta.dst_ids, device))
-    out = nsd.verify_attention(lay.q, kp, vp, i32(meta.block_table, device),
-                               i32(meta.seq_lens, device), i32(meta.q_indptr, device),
-                               meta.max_q, meta.max_seq_len)
+    kp, vp, out = _attend(meta, lay, device, fused)
     torch.cuda.synchronize()
     _gather_check(meta, lay, kp, vp, full=False, seed=layer)
     worst = check_attention(meta, lay, out, _sample_requests(meta, k=2, seed=layer))
