@@ -1,11 +1,13 @@
 """Benchmark: one verification round per step on one MI355X.
 
-A step is the whole hot path on one batch: kv_gather of the arriving
-requests' blocks, verify_attention over every layer, spec_accept.  Inputs
-(synthetic, seeded) are resident in HBM before timing starts.  Prints ONE JSON
-line; see DESIGN.md for the byte accounting behind "roofline".
+A step is the whole hot path on one batch: the KV-state preparation of the
+arriving requests' blocks fused with verification attention (one pass that
+reads each staged byte once), then spec_accept.  --unfused runs kv_gather and
+verify_attention as two kernels instead.  Inputs (synthetic, seeded) are
+resident in HBM before timing starts.  Prints ONE JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--workload verify_8b] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload verify_8b] [--unfused]
+                    [--no-cpu-baseline]
 """
 import argparse
 import json
@@ -28,22 +30,24 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="verify_8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--unfused", action="store_true",
+                    help="kv_gather and verify_attention as separate kernels")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy three times (counter calibration)")
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "verify_attention_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_29364_amd", "csrc", "verify_attention.hip")
 
 
-def measured_traffic(kernel_src):
-    """HBM bytes per verify_attention call from the committed counter runs, or None
+def measured_traffic(kernel):
+    """HBM bytes per call of `kernel` from the committed counter runs, or None
     when the kernel source has changed since those counters were taken."""
     import hashlib
     try:
-        rec = json.load(open(TRAFFIC_FILE))
-        digest = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+        rec = json.load(open(os.path.join(ROOT, "profiles", f"{kernel}_traffic.json")))
+        digest = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
     except (OSError, ValueError):
         return None
     if rec.get("kernel_sha256") != digest:
@@ -72,17 +76,30 @@ def describe(cfg):
 
 
 def algorithmic_bytes(cfg, meta, acc_len=None):
-    """Bytes each step must move at minimum (read + write), per kernel."""
+    """Bytes each kernel must move at minimum (read + write), per step.
+
+    gather: every staged block read and written (both planes).  attention:
+    every visible K/V token of every request read once, Q read, O written.
+    fused: the staged blocks read once and written once, the resident
+    requests' tokens read once, Q read, O written.  accept: the target and
+    draft rows acceptance reads (two rows at a rejection, the bonus row
+    otherwise), the uniforms, tokens and outputs."""
     hkv, d, hq = cfg.num_kv_heads, cfg.head_dim, cfg.num_q_heads
-    block_bytes = hkv * 16 * d * 2
-    gather = 2 * meta.n_pairs * 2 * block_bytes * cfg.num_layers
+    block_bytes = hkv * 16 * d * 2          # one plane of one block
+    token_bytes = 2 * hkv * d * 2           # K and V of one token, all KV heads
+    qo = 2 * meta.total_q * hq * d * 2
+    staged = 2 * meta.n_pairs * block_bytes  # both planes
+    gather = 2 * staged
     kv_tokens = int(meta.seq_lens.astype(np.int64).sum())
-    attn = cfg.num_layers * (kv_tokens * 2 * hkv * d * 2 + 2 * meta.total_q * hq * d * 2)
+    resident_tokens = int(meta.seq_lens[~meta.arriving].astype(np.int64).sum())
+    attn = kv_tokens * token_bytes + qo
+    fused = resident_tokens * token_bytes + 2 * staged + qo
     accept = 0
     if cfg.vocab and acc_len is not None:
         rows = np.where(acc_len < meta.depth, 2, 1).sum()
         accept = int(rows) * cfg.vocab * 4 + meta.total_q * 4 * 3
-    return gather, attn, accept
+    L = cfg.num_layers
+    return {"gather": L * gather, "attention": L * attn, "fused": L * fused, "accept": accept}
 
 
 def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
@@ -164,6 +181,7 @@ def main():
     bt, sl, qi = i32(meta.block_table), i32(meta.seq_lens), i32(meta.q_indptr)
     kp, vp = layer.k_pool, layer.v_pool
     ks, vs = layer.k_stage, layer.v_stage
+    st = i32(meta.stage_table)
     out = torch.empty_like(layer.q)
     ws_n = nsd.verify_attention_workspace_size(cfg.bs, cfg.num_q_heads, cfg.num_kv_heads,
                                                cfg.head_dim, meta.max_q, meta.max_seq_len)
@@ -174,10 +192,15 @@ def main():
 
     def step(ev=None):
         if ev: ev[0].record(stream)
-        nsd.kv_gather(ks, vs, kp, vp, src, dst)
+        if args.unfused:
+            nsd.kv_gather(ks, vs, kp, vp, src, dst)
         if ev: ev[1].record(stream)
-        nsd.verify_attention(layer.q, kp, vp, bt, sl, qi, meta.max_q, meta.max_seq_len,
-                             out=out, workspace=ws)
+        if args.unfused:
+            nsd.verify_attention(layer.q, kp, vp, bt, sl, qi, meta.max_q, meta.max_seq_len,
+                                 out=out, workspace=ws)
+        else:
+            nsd.gather_verify_attention(layer.q, kp, vp, ks, vs, bt, st, sl, qi, meta.max_q,
+                                        meta.max_seq_len, out=out, workspace=ws)
         if ev: ev[2].record(stream)
         if acc_in is not None:
             nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
@@ -203,8 +226,12 @@ def main():
                       for e in evs])
     g_ms, a_ms, c_ms = parts.mean(0)
     acc_host = acc_len.cpu().numpy() if acc_in is not None else None
-    gb, ab, cb = algorithmic_bytes(cfg, meta, acc_host)
-    achieved = ab / (a_ms * 1e-3) / 1e9
+    alg = algorithmic_bytes(cfg, meta, acc_host)
+    # the dominant kernel: the fused pass, or attention when run unfused
+    kern = "verify_attention" if args.unfused else "gather_verify_attention"
+    kb = alg["attention"] if args.unfused else alg["fused"]
+    step_bytes = (alg["gather"] + alg["attention"] if args.unfused else alg["fused"]) + alg["accept"]
+    achieved = kb / (a_ms * 1e-3) / 1e9
     result = {
         "metric": "verify-round requests/s (8B-shaped layer, bs=256, K=4); achieved HBM TB/s",
         "value": round(cfg.bs / (ms_step * 1e-3), 1),
@@ -214,16 +241,19 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": describe(cfg),
-        "breakdown_ms": {"kv_gather": round(g_ms, 5), "verify_attention": round(a_ms, 5),
-                         "spec_accept": round(c_ms, 5)},
-        "round_hbm_tbs": round((gb + ab + cb) / (ms_step * 1e-3) / 1e12, 3),
-        "gather_attention_tbs": round((gb + ab) / ((g_ms + a_ms) * 1e-3) / 1e12, 3),
-        "roofline": {"bound": "hbm", "kernel": "verify_attention", "achieved": round(achieved, 1),
+        "path": "unfused" if args.unfused else "fused",
+        "breakdown_ms": ({"kv_gather": round(g_ms, 5)} if args.unfused else {}) |
+                        {kern: round(a_ms, 5), "spec_accept": round(c_ms, 5)},
+        "round_hbm_tbs": round(step_bytes / (ms_step * 1e-3) / 1e12, 3),
+        # the KV-state preparation plus attention work, counted as the two
+        # separate kernels would move it, over the time the path took for it
+        "gather_attention_tbs": round((alg["gather"] + alg["attention"]) /
+                                      ((g_ms + a_ms) * 1e-3) / 1e12, 3),
+        "roofline": {"bound": "hbm", "kernel": kern, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(os.path.join(
-                         ROOT, "paper_2609_29364_amd", "csrc", "verify_attention.hip")),
-                     "alg_bytes_per_launch": ab},
+                     "traffic": measured_traffic(kern),
+                     "alg_bytes_per_launch": kb},
         "wall_s_timed": round(t_wall, 3),
     }
     if not args.no_cpu_baseline:

@@ -132,8 +132,9 @@ size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
  * q        : device, bf16 [total_q][num_q_heads][head_dim], total_q = q_indptr[bs].
  * k_cache, v_cache : device, this layer's planes, [num_blocks][...] (layout above).
  * block_table : device, int32 [bs][max_blocks_per_seq]; entries past
- *               ceil(L_r/16) are not read.  Ids outside [0, num_blocks) make
- *               their block's tokens invisible.
+ *               ceil(L_r/16) do not affect the result.  Ids outside
+ *               [0, num_blocks) make their block's tokens invisible.
+ *               num_blocks * num_kv_heads must not exceed 2^31 - 1.
  * seq_lens : device, int32 [bs], 1 <= L_r <= max_seq_len, L_r <= 16*max_blocks_per_seq.
  * q_indptr : device, int32 [bs+1], non-decreasing, q_indptr[0] = 0,
  *            1 <= n_q <= min(max_q_per_seq, L_r).
@@ -141,11 +142,9 @@ size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
  * head_dim in {64, 128}; block_size == 16.
  * scale : the softmax scale (usually 1/sqrt(head_dim)), finite.
  * out : device, bf16 [total_q][num_q_heads][head_dim]; may not alias q or the caches.
- * workspace : device, at least nsd_verify_attention_workspace_size(...) bytes.
- *             Zero-fill it once before its first use; every call leaves it
- *             ready for the next (a work counter at its start returns to zero
- *             when the call's kernels end).  Calls sharing a workspace must be
- *             ordered on one stream.
+ * workspace : device, at least nsd_verify_attention_workspace_size(...) bytes,
+ *             any contents (each call writes what it reads).  Calls sharing a
+ *             workspace must be ordered on one stream.
  * 1 <= bs <= 8192 (bs == 0 is a no-op returning NSD_OK).
  */
 nsd_status nsd_verify_attention(const void* q, const void* k_cache, const void* v_cache,
@@ -176,9 +175,11 @@ nsd_status nsd_verify_attention(const void* q, const void* k_cache, const void* 
  * nsd_kv_gather with the pairs (stage_table[r][b], block_table[r][b]) would:
  * each staged byte is read from HBM once.  The caches are therefore read and
  * written (non-const); the blocks of different requests must be distinct.
- * stage_num_blocks == 0 treats every request as resident.  Staging ids
- * outside [0, stage_num_blocks) make their tokens invisible; destination ids
- * outside [0, num_blocks) are not written.
+ * stage_num_blocks == 0 treats every request as resident.  A staging id
+ * outside [0, stage_num_blocks) makes its block's tokens invisible and the
+ * block is not written (as nsd_kv_gather skips such a pair); destination ids
+ * outside [0, num_blocks) are not written.  num_blocks * num_kv_heads and
+ * stage_num_blocks * num_kv_heads must not exceed 2^31 - 1.
  */
 nsd_status nsd_gather_verify_attention(const void* q, void* k_cache, void* v_cache,
                                        int64_t num_blocks, const void* k_stage,

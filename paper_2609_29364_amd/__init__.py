@@ -122,8 +122,9 @@ def verify_attention_workspace_size(bs, num_q_heads, num_kv_heads, head_dim, max
 
 
 def new_workspace(nbytes, device):
-    """A verify_attention workspace: zero-filled once, reusable by later calls on its stream."""
-    return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+    """A verify_attention workspace (no initialisation needed), reusable by later calls on
+    its stream."""
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 
 
 def verify_attention(q, k_cache, v_cache, block_table, seq_lens, q_indptr, max_q_per_seq,

@@ -26,6 +26,10 @@
 // * K/V are streamed once, so they are loaded non-temporally.  The registers
 //   loaded for one span are exactly the tile bytes, so the fused variant
 //   stores them back unchanged into the worker pool.
+// * A main-loop step covers NB blocks (NB * 16 tokens).  A wave's throughput
+//   is bounded by the K/V bytes it keeps in flight over the HBM latency, so
+//   tiles whose registers allow it take four blocks (32 KiB of K and V per
+//   step for head_dim 128) and run one wave per SIMD.
 // * Software pipeline: within an item K(j+1) is requested as soon as S(j)
 //   consumed K(j) and V(j+1) as soon as PV(j) consumed V(j); across items the
 //   next item's first span is requested during the current item's last span
@@ -35,7 +39,8 @@
 //   compiler wait for all outstanding loads at the join).
 // * Load balance (stream-K): the spans of all (request, KV head) items are cut
 //   into as many equal contiguous ranges as the device keeps waves resident,
-//   whatever the spread of context lengths.  Items cut by a range boundary
+//   whatever the spread of context lengths.  The split is static: the
+//   workspace needs no initialisation and no wave waits on another.  Items cut by a range boundary
 //   leave partials that a small second kernel merges in range order
 //   (deterministic, no atomics in the arithmetic); all other items are
 //   written directly.
@@ -58,9 +63,12 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 
 constexpr int kBlock = 16;        // token slots per KV block
-constexpr int kSpan = 32;         // tokens per main-loop step
 constexpr int kMaxRows = 64;      // (Hq/Hkv) * max_q_per_seq limit
 constexpr int kMaxBatch = 8192;   // the span prefix of the batch lives in LDS
+
+// Blocks per main-loop step for a (head_dim, row tiles) instantiation: four
+// where the registers of two extra K/V tiles fit beside the accumulators.
+__host__ __device__ constexpr int span_blocks(int d, int mt) { return d * mt <= 256 ? 4 : 2; }
 
 struct Params {
   const uint16_t* q;
@@ -78,10 +86,9 @@ struct Params {
   float* part_o;       // [2 * ranges][MT*16][D]: head/tail partial O per range
   float2* part_ml;     // [2 * ranges][MT*16]: (running max, sum)
   uint32_t* prefix;    // [bs+1]: exclusive prefix of per-request span counts
-  uint32_t* counters;  // [1]: next dynamic chunk to claim (zero between dispatches)
   uint16_t* trash;     // one K tile + one V tile that absorb stores to invalid ids
-  int64_t num_blocks;
-  int64_t stage_blocks;
+  int32_t num_blocks;    // blocks in the worker pool (tiles fit 32-bit indexes)
+  int32_t stage_blocks;  // blocks in the staging pool (0 without fusion)
   int32_t bs;
   int32_t max_blocks_per_seq;
   int32_t num_q_heads;
@@ -93,14 +100,14 @@ struct Params {
   float scale_log2;  // softmax scale * log2(e)
 };
 
-template <int D>
+template <int D, int NB>
 struct KOps {
-  u32x4 k[2][D / 32];   // K operands of a span's two blocks
+  u32x4 k[NB][D / 32];  // K operands of a span's NB blocks
 };
 
-template <int D>
+template <int D, int NB>
 struct VOps {
-  u32x2 v[2][D / 16];   // V^T operand halves of a span's two blocks
+  u32x2 v[NB][D / 16];  // V^T operand halves of a span's NB blocks
 };
 
 template <int MT, int D>
@@ -118,14 +125,39 @@ __device__ inline int64_t uniform64(int64_t x) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+// Reductions over the four 16-lane rows of a wave (lanes l, l^16, l^32 and
+// l^48 hold the same query row): two cross-row register swaps, no LDS.
+// Swapping a register with a copy of itself leaves, in every lane, its own
+// value and its row partner's in the two registers.  The instruction is
+// written out because the compiler's builtin for it merges the two results;
+// the nops cover the VALU-write to cross-lane-read hazard on both sides.  The
+// sum pairs (l, l^32) first, so every lane of a row adds the same two halves.
+struct Pair {
+  float a, b;
+};
+
+__device__ inline Pair swap32(float x) {
+  Pair r = {x, x};
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(r.a), "+v"(r.b));
+  return r;
+}
+
+__device__ inline Pair swap16(float x) {
+  Pair r = {x, x};
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(r.a), "+v"(r.b));
+  return r;
+}
+
 __device__ inline float wave_max_groups(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  return fmaxf(x, __shfl_xor(x, 32));
+  const Pair a = swap32(x);
+  const Pair b = swap16(fmaxf(a.a, a.b));
+  return fmaxf(b.a, b.b);
 }
 
 __device__ inline float wave_sum_groups(float x) {
-  x += __shfl_xor(x, 16);
-  return x + __shfl_xor(x, 32);
+  const Pair a = swap32(x);
+  const Pair b = swap16(a.a + a.b);
+  return b.a + b.b;
 }
 
 __device__ inline uint32_t keep_mask(int n_valid_elems) {
@@ -140,7 +172,10 @@ __device__ inline int clamp_len(const Params& p, const int32_t* __restrict__ seq
 
 // Spans of one (request, KV head) item; an empty context still owns one span
 // so that its rows are written (as zeros).
-__device__ inline int spans_of(int L) { return max(1, (L + kSpan - 1) / kSpan); }
+template <int NB>
+__device__ inline int spans_of(int L) {
+  return max(1, (L + NB * kBlock - 1) / (NB * kBlock));
+}
 
 // One (request r, KV head g) item restricted to spans [j0, j1) of a range.
 struct Item {
@@ -149,7 +184,7 @@ struct Item {
   bool arriving;     // fused variant: K/V come from the staging pool
 };
 
-template <bool FUSE>
+template <int NB, bool FUSE>
 __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
                                  const int32_t* __restrict__ stage_table, int r, int64_t pr,
@@ -158,7 +193,7 @@ __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ se
   it.r = r;
   it.pr = pr;
   it.L = clamp_len(p, seq_lens, r);
-  it.n = spans_of(it.L);
+  it.n = spans_of<NB>(it.L);
   it.qo = q_indptr[r];
   it.nq = max(0, min(q_indptr[r + 1] - it.qo, p.max_q));
   const int64_t off = s - (int64_t)p.num_kv_heads * pr;
@@ -172,114 +207,131 @@ __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ se
   return it;
 }
 
+// Raw block-table entries of one span (scalar loads, checked later).
+template <int NB>
+struct SpanIds {
+  int32_t src[NB];   // ids the tiles are read from (worker pool, or staging if arriving)
+  int32_t dst[NB];   // worker-pool ids the fused variant writes
+};
+
+template <int NB>
 struct SpanRef {
   const uint16_t* k_src;  // planes the span is read from (pool or staging)
   const uint16_t* v_src;
-  int64_t hs0, hs1;       // element offsets of the two source tiles
-  int64_t hd0, hd1;       // element offsets of the two destination tiles (fused)
+  int32_t ts[NB];         // source tiles (block * num_kv_heads + head)
+  int32_t td[NB];         // destination tiles (fused); -1: the trash tiles
   int32_t t;              // first token of the span
-  bool bad0, bad1;        // block id out of range: tokens invisible
-  bool has1;              // the span's second block exists
+  uint32_t bad;           // bit b: block b's id is out of range (its tokens are invisible)
 };
 
-// Span j of item it.  Block ids are wave-uniform, so they are fetched with
-// scalar loads, which keep the vector-memory counter free for the K/V stream.
-template <int D, bool FUSE>
-__device__ inline SpanRef span_ref(const Params& p, const int32_t* __restrict__ block_table,
-                                   const int32_t* __restrict__ stage_table, const Item& it,
-                                   int j) {
-  SpanRef s;
-  s.t = j * kSpan;
-  const int b0 = s.t / kBlock;
-  s.has1 = s.t + kBlock < it.L;
+// Table entries of span j of item it.  Block ids are wave-uniform, so they
+// are fetched with scalar loads, which keep the vector-memory counter free
+// for the K/V stream; the indexes are clamped into the row, so the loads are
+// unconditional.
+template <int NB, bool FUSE>
+__device__ inline SpanIds<NB> load_ids(const Params& p, const int32_t* __restrict__ block_table,
+                                       const int32_t* __restrict__ stage_table, const Item& it,
+                                       int j) {
+  SpanIds<NB> ids;
   const int64_t row = (int64_t)it.r * p.max_blocks_per_seq;
-  const int64_t tile = (int64_t)D * kBlock;
-  int32_t id0 = block_table[row + b0];
-  int32_t id1 = s.has1 ? block_table[row + b0 + 1] : id0;
-  const bool pbad0 = id0 < 0 || id0 >= p.num_blocks;
-  const bool pbad1 = id1 < 0 || id1 >= p.num_blocks;
-  if (FUSE && it.arriving) {
-    int32_t sid0 = stage_table[row + b0];
-    int32_t sid1 = s.has1 ? stage_table[row + b0 + 1] : sid0;
-    s.bad0 = sid0 < 0 || sid0 >= p.stage_blocks;
-    const bool sbad1 = sid1 < 0 || sid1 >= p.stage_blocks;
-    s.bad1 = s.has1 && sbad1;
-    if (s.bad0) sid0 = 0;
-    if (!s.has1 || sbad1) sid1 = sid0;
-    s.k_src = p.k_stage;
-    s.v_src = p.v_stage;
-    s.hs0 = ((int64_t)sid0 * p.num_kv_heads + it.g) * tile;
-    s.hs1 = ((int64_t)sid1 * p.num_kv_heads + it.g) * tile;
-    // destinations outside the pool are redirected to the trash tile
-    s.hd0 = pbad0 ? -1 : ((int64_t)id0 * p.num_kv_heads + it.g) * tile;
-    s.hd1 = (pbad1 || !s.has1) ? -1 : ((int64_t)id1 * p.num_kv_heads + it.g) * tile;
-  } else {
-    s.bad0 = pbad0;
-    s.bad1 = s.has1 && pbad1;
-    if (pbad0) id0 = 0;
-    if (!s.has1 || pbad1) id1 = id0;
-    s.k_src = p.k_cache;
-    s.v_src = p.v_cache;
-    s.hs0 = ((int64_t)id0 * p.num_kv_heads + it.g) * tile;
-    s.hs1 = ((int64_t)id1 * p.num_kv_heads + it.g) * tile;
-    s.hd0 = s.hd1 = -1;
+  const int last = p.max_blocks_per_seq - 1;
+  const int32_t* __restrict__ src = (FUSE && it.arriving) ? stage_table : block_table;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int e = min(j * NB + b, last);
+    ids.src[b] = src[row + e];
+    ids.dst[b] = FUSE ? block_table[row + e] : -1;
+  }
+  return ids;
+}
+
+// Span j of item it from its table entries.  Blocks past the context reuse
+// block 0's tile (their tokens are masked) and send fused stores to the trash
+// tiles, as do arriving blocks with an invalid staging or destination id.
+template <int NB, bool FUSE>
+__device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
+                                       const SpanIds<NB>& ids) {
+  SpanRef<NB> s;
+  s.t = j * NB * kBlock;
+  s.bad = 0;
+  const int nb = max(1, min(NB, (it.L - s.t + kBlock - 1) / kBlock));
+  const bool arr = FUSE && it.arriving;
+  s.k_src = arr ? p.k_stage : p.k_cache;
+  s.v_src = arr ? p.v_stage : p.v_cache;
+  const int32_t src_blocks = arr ? p.stage_blocks : p.num_blocks;
+  int32_t ts0 = 0;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int32_t sid = ids.src[b];
+    const bool here = b < nb;
+    const bool sbad = sid < 0 || sid >= src_blocks;
+    if (here && sbad) s.bad |= 1u << b;
+    const int32_t ts = (sbad ? 0 : sid) * p.num_kv_heads + it.g;
+    if (b == 0) ts0 = ts;
+    s.ts[b] = (here && !sbad) ? ts : ts0;
+    const int32_t did = ids.dst[b];
+    const bool dbad = did < 0 || did >= p.num_blocks;
+    s.td[b] = (arr && here && !sbad && !dbad) ? did * p.num_kv_heads + it.g : -1;
   }
   return s;
 }
 
-template <int D>
-__device__ inline void load_k(KOps<D>& o, const SpanRef& s, int lane) {
+template <int D, int NB>
+__device__ inline void load_k(KOps<D, NB>& o, const SpanRef<NB>& s, int lane) {
   const int row = lane & 15, grp = lane >> 4;
-  const uint16_t* k0 = s.k_src + s.hs0;
-  const uint16_t* k1 = s.k_src + s.hs1;
 #pragma unroll
   for (int kk = 0; kk < D / 32; ++kk) {
     const int off = ((kk * 4 + grp) * kBlock + row) * 8;
-    o.k[0][kk] = __builtin_nontemporal_load((const u32x4*)(k0 + off));
-    o.k[1][kk] = __builtin_nontemporal_load((const u32x4*)(k1 + off));
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      o.k[b][kk] = __builtin_nontemporal_load(
+          (const u32x4*)(s.k_src + (int64_t)s.ts[b] * (D * kBlock) + off));
   }
 }
 
-template <int D>
-__device__ inline void load_v(VOps<D>& o, const SpanRef& s, int lane) {
+template <int D, int NB>
+__device__ inline void load_v(VOps<D, NB>& o, const SpanRef<NB>& s, int lane) {
   const int row = lane & 15, grp = lane >> 4;
-  const uint16_t* v0 = s.v_src + s.hs0;
-  const uint16_t* v1 = s.v_src + s.hs1;
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) {
     const int off = (dt * 16 + row) * kBlock + grp * 4;
-    o.v[0][dt] = __builtin_nontemporal_load((const u32x2*)(v0 + off));
-    o.v[1][dt] = __builtin_nontemporal_load((const u32x2*)(v1 + off));
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      o.v[b][dt] = __builtin_nontemporal_load(
+          (const u32x2*)(s.v_src + (int64_t)s.ts[b] * (D * kBlock) + off));
   }
 }
 
 // Fused variant: the loaded tiles go back out unchanged to the worker pool
 // (same offsets inside the tile as they were read from).
-template <int D>
-__device__ inline void store_k(const KOps<D>& o, const Params& p, const SpanRef& s, bool second,
+template <int D, int NB>
+__device__ inline void store_k(const KOps<D, NB>& o, const Params& p, const SpanRef<NB>& s,
                                int lane) {
   const int row = lane & 15, grp = lane >> 4;
-  uint16_t* k0 = s.hd0 >= 0 ? p.k_dst + s.hd0 : p.trash;
-  uint16_t* k1 = s.hd1 >= 0 ? p.k_dst + s.hd1 : p.trash;
 #pragma unroll
-  for (int kk = 0; kk < D / 32; ++kk) {
-    const int off = ((kk * 4 + grp) * kBlock + row) * 8;
-    __builtin_nontemporal_store(o.k[0][kk], (u32x4*)(k0 + off));
-    if (second) __builtin_nontemporal_store(o.k[1][kk], (u32x4*)(k1 + off));
+  for (int b = 0; b < NB; ++b) {
+    uint16_t* dst = s.td[b] >= 0 ? p.k_dst + (int64_t)s.td[b] * (D * kBlock) : p.trash;
+#pragma unroll
+    for (int kk = 0; kk < D / 32; ++kk) {
+      const int off = ((kk * 4 + grp) * kBlock + row) * 8;
+      __builtin_nontemporal_store(o.k[b][kk], (u32x4*)(dst + off));
+    }
   }
 }
 
-template <int D>
-__device__ inline void store_v(const VOps<D>& o, const Params& p, const SpanRef& s, bool second,
+template <int D, int NB>
+__device__ inline void store_v(const VOps<D, NB>& o, const Params& p, const SpanRef<NB>& s,
                                int lane) {
   const int row = lane & 15, grp = lane >> 4;
-  uint16_t* v0 = s.hd0 >= 0 ? p.v_dst + s.hd0 : p.trash + D * kBlock;
-  uint16_t* v1 = s.hd1 >= 0 ? p.v_dst + s.hd1 : p.trash + D * kBlock;
 #pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    const int off = (dt * 16 + row) * kBlock + grp * 4;
-    __builtin_nontemporal_store(o.v[0][dt], (u32x2*)(v0 + off));
-    if (second) __builtin_nontemporal_store(o.v[1][dt], (u32x2*)(v1 + off));
+  for (int b = 0; b < NB; ++b) {
+    uint16_t* dst =
+        s.td[b] >= 0 ? p.v_dst + (int64_t)s.td[b] * (D * kBlock) : p.trash + D * kBlock;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const int off = (dt * 16 + row) * kBlock + grp * 4;
+      __builtin_nontemporal_store(o.v[b][dt], (u32x2*)(dst + off));
+    }
   }
 }
 
@@ -303,36 +355,38 @@ __device__ inline void load_q(QOps<MT, D>& o, const Params& p, const Item& it, i
   }
 }
 
+// Rows past the item's rows become zeros once their Q is current.
 template <int D, int MT>
-__device__ inline void stage_q(u32x4* qlds, const QOps<MT, D>& o, const Item& it, int lane) {
+__device__ inline void mask_q(QOps<MT, D>& o, const Item& it, int lane) {
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const bool valid = mt * 16 + (lane & 15) < it.rows;
 #pragma unroll
     for (int kk = 0; kk < D / 32; ++kk)
-      qlds[(mt * (D / 32) + kk) * 64 + lane] = valid ? o.q[mt][kk] : u32x4{0, 0, 0, 0};
+      o.q[mt][kk] = valid ? o.q[mt][kk] : u32x4{0, 0, 0, 0};
   }
 }
 
-// S^T[token][row] of the span's two blocks.  Q operands come from this
-// wave's LDS copy, stored in operand order: one 16-byte run per lane per
-// (row tile, k-step), so every read is conflict-free.
-template <int D, int MT>
-__device__ inline void span_scores(const KOps<D>& k, const u32x4* qlds, int lane,
-                                   f32x4 (&st)[2][MT]) {
+// S^T[token][row] of the span's NB blocks; the item's Q operands stay in
+// registers.
+template <int D, int MT, int NB>
+__device__ inline void span_scores(const KOps<D, NB>& k, const QOps<MT, D>& q,
+                                   f32x4 (&st)[NB][MT]) {
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0;
+    f32x4 c[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) c[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < D / 32; ++kk) {
-      const bf16x8 qo = __builtin_bit_cast(bf16x8, qlds[(mt * (D / 32) + kk) * 64 + lane]);
-      c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, k.k[0][kk]), qo,
-                                                   c0, 0, 0, 0);
-      c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, k.k[1][kk]), qo,
-                                                   c1, 0, 0, 0);
+      const bf16x8 qo = __builtin_bit_cast(bf16x8, q.q[mt][kk]);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        c[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, k.k[b][kk]),
+                                                       qo, c[b], 0, 0, 0);
     }
-    st[0][mt] = c0;
-    st[1][mt] = c1;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) st[b][mt] = c[b];
   }
 }
 
@@ -344,101 +398,123 @@ struct Acc {
   int pos[MT];
 };
 
-// Online-softmax update from one span's scores; returns P^T operands (bf16).
-template <int D, int MT>
-__device__ inline void span_softmax(const f32x4 (&st)[2][MT], const SpanRef& s, Acc<D, MT>& a,
-                                    int win, float scale_log2, int lane, bf16x8 (&pop)[MT]) {
+// Online-softmax update from one span's scores; returns the P^T operands
+// (bf16), one per pair of blocks: a 32-token k-step whose lane holds 4 tokens
+// of each block of the pair, as the S^T accumulators left them.
+template <int D, int MT, int NB>
+__device__ inline void span_softmax(const f32x4 (&st)[NB][MT], const SpanRef<NB>& s,
+                                    Acc<D, MT>& a, int win, float scale_log2, int lane,
+                                    bf16x8 (&pop)[NB / 2][MT]) {
   const int grp = lane >> 4;
-  const bool need_mask = (s.t + kSpan > win) || s.bad0 || s.bad1;
+  const bool need_mask = (s.t + NB * kBlock > win) || s.bad;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    float x[2][4];
+    float x[NB][4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[h][i] = st[h][mt][i] * scale_log2;
+      for (int i = 0; i < 4; ++i) x[b][i] = st[b][mt][i] * scale_log2;
     if (need_mask) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const bool bad = h ? s.bad1 : s.bad0;
+      for (int b = 0; b < NB; ++b) {
+        const bool bad = (s.bad >> b) & 1u;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int t = s.t + h * kBlock + grp * 4 + i;
-          x[h][i] = (t <= a.pos[mt] && !bad) ? x[h][i] : -INFINITY;
+          const int t = s.t + b * kBlock + grp * 4 + i;
+          x[b][i] = (t <= a.pos[mt] && !bad) ? x[b][i] : -INFINITY;
         }
       }
     }
     float mx = x[0][0];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, x[h][i]);
+      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, x[b][i]);
     mx = wave_max_groups(mx);
     const float m_new = fmaxf(a.m[mt], mx);
     const bool none = m_new == -INFINITY;
     const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(a.m[mt] - m_new);
     const float msub = none ? 0.f : m_new;
-    float pr[2][4];
+    float pr[NB][4];
     float psum = 0.f;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        pr[h][i] = __builtin_amdgcn_exp2f(x[h][i] - msub);
-        psum += pr[h][i];
+        pr[b][i] = __builtin_amdgcn_exp2f(x[b][i] - msub);
+        psum += pr[b][i];
       }
     a.l[mt] = a.l[mt] * alpha + psum;
     a.m[mt] = m_new;
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) a.o[mt][dt] *= alpha;
-    pop[mt] = bf16x8{(__bf16)pr[0][0], (__bf16)pr[0][1], (__bf16)pr[0][2], (__bf16)pr[0][3],
-                     (__bf16)pr[1][0], (__bf16)pr[1][1], (__bf16)pr[1][2], (__bf16)pr[1][3]};
+#pragma unroll
+    for (int kp = 0; kp < NB / 2; ++kp) {
+      const float(&u)[4] = pr[2 * kp];
+      const float(&w)[4] = pr[2 * kp + 1];
+      pop[kp][mt] = bf16x8{(__bf16)u[0], (__bf16)u[1], (__bf16)u[2], (__bf16)u[3],
+                           (__bf16)w[0], (__bf16)w[1], (__bf16)w[2], (__bf16)w[3]};
+    }
   }
 }
 
 // O^T += V^T P^T; V elements of tokens >= L (or of bad blocks) are zeroed.
-template <int D, int MT>
-__device__ inline void span_pv(const VOps<D>& v, const SpanRef& s, int L, const bf16x8 (&pop)[MT],
-                               Acc<D, MT>& a, int lane) {
+template <int D, int MT, int NB>
+__device__ inline void span_pv(const VOps<D, NB>& v, const SpanRef<NB>& s, int L,
+                               const bf16x8 (&pop)[NB / 2][MT], Acc<D, MT>& a, int lane) {
   const int grp = lane >> 4;
-  uint32_t keep[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
-  if (s.t + kSpan > L || s.bad0 || s.bad1) {
+  uint32_t keep[NB][2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const bool bad = h ? s.bad1 : s.bad0;
-      const int nv = bad ? 0 : min(4, max(0, L - (s.t + h * kBlock + grp * 4)));
-      keep[2 * h] = keep_mask(nv);
-      keep[2 * h + 1] = keep_mask(nv - 2);
+  for (int b = 0; b < NB; ++b) keep[b][0] = keep[b][1] = 0xffffffffu;
+  if (s.t + NB * kBlock > L || s.bad) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const bool bad = (s.bad >> b) & 1u;
+      const int nv = bad ? 0 : min(4, max(0, L - (s.t + b * kBlock + grp * 4)));
+      keep[b][0] = keep_mask(nv);
+      keep[b][1] = keep_mask(nv - 2);
     }
   }
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) {
-    const u32x4 w = {v.v[0][dt].x & keep[0], v.v[0][dt].y & keep[1], v.v[1][dt].x & keep[2],
-                     v.v[1][dt].y & keep[3]};
-    const bf16x8 vop = __builtin_bit_cast(bf16x8, w);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-      a.o[mt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[mt], a.o[mt][dt], 0, 0, 0);
+    for (int kp = 0; kp < NB / 2; ++kp) {
+      const u32x2 v0 = v.v[2 * kp][dt], v1 = v.v[2 * kp + 1][dt];
+      const u32x4 w = {v0.x & keep[2 * kp][0], v0.y & keep[2 * kp][1],
+                       v1.x & keep[2 * kp + 1][0], v1.y & keep[2 * kp + 1][1]};
+      const bf16x8 vop = __builtin_bit_cast(bf16x8, w);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        a.o[mt][dt] =
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[kp][mt], a.o[mt][dt], 0, 0, 0);
+    }
   }
 }
 
 // One span: S from K, online softmax, PV from V.  The registers each phase
-// has consumed are refilled at once with span `nr`; with STORE (fused
-// variant, arriving item) the loaded tiles are first written to the pool
-// (SECOND: the span's second block exists).
-template <int D, int MT, bool STORE, bool SECOND>
-__device__ inline void span_step(KOps<D>& kr, VOps<D>& vr, const SpanRef& sr, const SpanRef& nr,
-                                 const u32x4* qlds, const Params& p, Acc<D, MT>& a, int win,
+// has consumed are refilled at once with span nj of item nit (whose table
+// entries were requested before this step, so their latency hides behind the
+// score products); with STORE (fused variant, arriving item) the loaded tiles
+// are first written to the pool.
+template <int D, int MT, int NB, bool FUSE, bool STORE>
+__device__ inline void span_step(KOps<D, NB>& kr, VOps<D, NB>& vr, SpanRef<NB>& cur,
+                                 const Item& nit, int nj, const SpanIds<NB>& nids,
+                                 const QOps<MT, D>& q, const Params& p, Acc<D, MT>& a, int win,
                                  int L, int lane) {
-  f32x4 st[2][MT];
-  span_scores<D, MT>(kr, qlds, lane, st);
-  if constexpr (STORE) store_k<D>(kr, p, sr, SECOND, lane);
-  load_k<D>(kr, nr, lane);
-  bf16x8 pop[MT];
-  span_softmax<D, MT>(st, sr, a, win, p.scale_log2, lane, pop);
-  span_pv<D, MT>(vr, sr, L, pop, a, lane);
-  if constexpr (STORE) store_v<D>(vr, p, sr, SECOND, lane);
-  load_v<D>(vr, nr, lane);
+  f32x4 st[NB][MT];
+  span_scores<D, MT, NB>(kr, q, st);
+  if constexpr (STORE) store_k<D, NB>(kr, p, cur, lane);
+  // keep the next span's address arithmetic (and the wait for its table
+  // entries) behind the score products
+  __builtin_amdgcn_sched_barrier(0);
+  const SpanRef<NB> nr = make_ref<NB, FUSE>(p, nit, nj, nids);
+  load_k<D, NB>(kr, nr, lane);
+  bf16x8 pop[NB / 2][MT];
+  span_softmax<D, MT, NB>(st, cur, a, win, p.scale_log2, lane, pop);
+  span_pv<D, MT, NB>(vr, cur, L, pop, a, lane);
+  if constexpr (STORE) store_v<D, NB>(vr, p, cur, lane);
+  load_v<D, NB>(vr, nr, lane);
+  cur = nr;
 }
 
 template <int D, int MT>
@@ -485,6 +561,7 @@ __device__ inline void finish_item(const Params& p, Acc<D, MT>& a, const Item& i
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = mt * 16 + (lane & 15);
+      if (m >= it.rows) continue;   // stores of unused rows cost far more than the branch
       float* dst = p.part_o + (slot * (MT * 16) + m) * D + grp * 4;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) *(f32x4*)(dst + dt * 16) = a.o[mt][dt];
@@ -493,30 +570,16 @@ __device__ inline void finish_item(const Params& p, Acc<D, MT>& a, const Item& i
   }
 }
 
-constexpr int kStaticPct = 100;  // share of spans split evenly over the waves up front
-constexpr int kChunkSpans = 8;   // spans per dynamically claimed chunk
-
 // The global sequence of T spans (ordered by request, then KV head, then
-// position) is cut into ranges: W static ranges covering the first Ts spans
-// evenly, one per wave, then C dynamic chunks of kChunkSpans spans that waves
-// claim from a counter once their static range is done.  Every kernel derives
-// the same ranges from T and W.
+// position) is cut into W equal contiguous ranges, one per resident wave.
+// Every kernel derives the same ranges from T and W.
 struct Ranges {
-  int64_t T, Ts, W, C;
-  __device__ Ranges(int64_t total, int64_t waves) : T(total), W(waves) {
-    Ts = total * kStaticPct / 100;
-    C = (total - Ts + kChunkSpans - 1) / kChunkSpans;
-  }
-  __device__ int64_t begin(int64_t rid) const {
-    return rid < W ? rid * Ts / W : Ts + (rid - W) * kChunkSpans;
-  }
-  __device__ int64_t end(int64_t rid) const {
-    return rid < W ? (rid + 1) * Ts / W : min(T, Ts + (rid - W + 1) * kChunkSpans);
-  }
+  int64_t T, W;
+  __device__ Ranges(int64_t total, int64_t waves) : T(total), W(waves) {}
+  __device__ int64_t begin(int64_t rid) const { return rid * T / W; }
+  __device__ int64_t end(int64_t rid) const { return (rid + 1) * T / W; }
   // range holding span s
-  __device__ int64_t of(int64_t s) const {
-    return s < Ts ? ((s + 1) * W - 1) / Ts : W + (s - Ts) / kChunkSpans;
-  }
+  __device__ int64_t of(int64_t s) const { return ((s + 1) * W - 1) / T; }
 };
 
 // Request whose spans [hkv*pre[r], hkv*pre[r+1]) contain global span s.
@@ -532,99 +595,107 @@ __device__ inline int find_request(const uint32_t* pre, int bs, int hkv, int64_t
 // Spans [j0, j1) of one item.  The loads of the item's first span were issued
 // by the caller; during its last span the first span of `next` is requested
 // (when the range ends inside `it`, `next` is `it` and the loads are spare).
-template <int D, int MT, bool FUSE, bool ARR>
+// Table entries of the span after span j of `it`: span j+1, or the first
+// span of `next` when j is the item's last.
+template <int NB, bool FUSE>
+__device__ inline SpanIds<NB> ids_after(const Params& p, const int32_t* __restrict__ block_table,
+                                        const int32_t* __restrict__ stage_table, const Item& it,
+                                        const Item& next, int j) {
+  return j + 1 < it.j1 ? load_ids<NB, FUSE>(p, block_table, stage_table, it, j + 1)
+                       : load_ids<NB, FUSE>(p, block_table, stage_table, next, next.j0);
+}
+
+// Spans [j0, j1) of one item.  The loads of the item's first span were issued
+// by the caller; during its last span the first span of `next` is requested
+// (when the range ends inside `it`, `next` is `it` and the loads are spare).
+// Table entries are fetched one step before the step that uses them.
+template <int D, int MT, int NB, bool FUSE, bool ARR>
 __device__ inline void run_item(const Params& p, const int32_t* __restrict__ block_table,
                                 const int32_t* __restrict__ stage_table, const Item& it,
-                                const Item& next, KOps<D>& kreg, VOps<D>& vreg, SpanRef& cur,
-                                const u32x4* qlds, Acc<D, MT>& a, int lane) {
+                                const Item& next, KOps<D, NB>& kreg, VOps<D, NB>& vreg,
+                                SpanRef<NB>& cur, const QOps<MT, D>& q, Acc<D, MT>& a,
+                                int lane) {
+  SpanIds<NB> ids = ids_after<NB, FUSE>(p, block_table, stage_table, it, next, it.j0);
   for (int j = it.j0; j + 1 < it.j1; ++j) {
-    const SpanRef nxt = span_ref<D, FUSE>(p, block_table, stage_table, it, j + 1);
-    span_step<D, MT, ARR, true>(kreg, vreg, cur, nxt, qlds, p, a, it.win, it.L, lane);
-    cur = nxt;
+    const SpanIds<NB> ids2 = ids_after<NB, FUSE>(p, block_table, stage_table, it, next, j + 1);
+    span_step<D, MT, NB, FUSE, ARR>(kreg, vreg, cur, it, j + 1, ids, q, p, a, it.win, it.L, lane);
+    ids = ids2;
   }
-  const SpanRef nxt = span_ref<D, FUSE>(p, block_table, stage_table, next, next.j0);
-  if (!ARR || cur.has1)
-    span_step<D, MT, ARR, true>(kreg, vreg, cur, nxt, qlds, p, a, it.win, it.L, lane);
-  else
-    span_step<D, MT, ARR, false>(kreg, vreg, cur, nxt, qlds, p, a, it.win, it.L, lane);
-  cur = nxt;
+  span_step<D, MT, NB, FUSE, ARR>(kreg, vreg, cur, next, next.j0, ids, q, p, a, it.win, it.L,
+                                  lane);
 }
 
 // One range [s, s1) of global spans, range id rid: online softmax over every
 // (request, KV head) item the range touches.
-template <int D, int MT, bool FUSE>
+template <int D, int MT, int NB, bool FUSE>
 __device__ void process_range(const Params& p, const int32_t* __restrict__ block_table,
                               const int32_t* __restrict__ stage_table,
                               const int32_t* __restrict__ seq_lens,
                               const int32_t* __restrict__ q_indptr, const uint32_t* pre,
-                              u32x4* qbuf0, u32x4* qbuf1, int total_q, int64_t rid, int64_t s,
+                              int total_q, int64_t rid, int64_t s,
                               int64_t s1, int lane) {
   const int hkv = p.num_kv_heads;
   const int r0 = uniform(find_request(pre, p.bs, hkv, s));
-  Item it = make_item<FUSE>(p, seq_lens, q_indptr, stage_table, r0, uniform64(pre[r0]), s, s1);
+  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, r0, uniform64(pre[r0]), s,
+                                s1);
   Item next = it;
   int64_t s_next = s + (it.j1 - it.j0);
   if (s_next < s1) {
     const bool nr = it.g == hkv - 1;
-    next = make_item<FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
-                           nr ? it.pr + it.n : it.pr, s_next, s1);
+    next = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
+                               nr ? it.pr + it.n : it.pr, s_next, s1);
   }
 
-  // Q of the next item is fetched one item ahead into registers when the
-  // tile leaves room for them (PREQ); larger tiles fetch it at the switch.
+  // Q of the next item is fetched one item ahead when the tile leaves room
+  // for a second copy (PREQ); larger tiles fetch it at the switch.
   constexpr bool PREQ = D * MT <= 256;
-  QOps<MT, D> qr;
-  load_q<D, MT>(qr, p, it, total_q, lane);
-  SpanRef cur = span_ref<D, FUSE>(p, block_table, stage_table, it, it.j0);
-  KOps<D> kreg;
-  VOps<D> vreg;
-  load_k<D>(kreg, cur, lane);
-  load_v<D>(vreg, cur, lane);
-  stage_q<D, MT>(qbuf0, qr, it, lane);
-  if constexpr (PREQ) load_q<D, MT>(qr, p, next, total_q, lane);
-  __builtin_amdgcn_wave_barrier();
-  u32x4* qcur = qbuf0;
-  u32x4* qnext = qbuf1;
+  QOps<MT, D> qc, qn;
+  load_q<D, MT>(qc, p, it, total_q, lane);
+  SpanRef<NB> cur =
+      make_ref<NB, FUSE>(p, it, it.j0, load_ids<NB, FUSE>(p, block_table, stage_table, it, it.j0));
+  KOps<D, NB> kreg;
+  VOps<D, NB> vreg;
+  load_k<D, NB>(kreg, cur, lane);
+  load_v<D, NB>(vreg, cur, lane);
+  mask_q<D, MT>(qc, it, lane);
+  if constexpr (PREQ) load_q<D, MT>(qn, p, next, total_q, lane);
   while (true) {
     Acc<D, MT> a;
     init_acc<D, MT>(a, p, it, lane);
     if (FUSE && it.arriving)
-      run_item<D, MT, FUSE, true>(p, block_table, stage_table, it, next, kreg, vreg, cur, qcur,
-                                  a, lane);
+      run_item<D, MT, NB, FUSE, true>(p, block_table, stage_table, it, next, kreg, vreg, cur,
+                                      qc, a, lane);
     else
-      run_item<D, MT, FUSE, false>(p, block_table, stage_table, it, next, kreg, vreg, cur, qcur,
-                                   a, lane);
+      run_item<D, MT, NB, FUSE, false>(p, block_table, stage_table, it, next, kreg, vreg, cur,
+                                       qc, a, lane);
     finish_item<D, MT>(p, a, it, rid, lane);
     if (s_next >= s1) break;
     // switch to the next item
-    if constexpr (!PREQ) load_q<D, MT>(qr, p, next, total_q, lane);
-    stage_q<D, MT>(qnext, qr, next, lane);
-    __builtin_amdgcn_wave_barrier();
-    u32x4* t = qcur;
-    qcur = qnext;
-    qnext = t;
+    if constexpr (PREQ) qc = qn;
+    else load_q<D, MT>(qc, p, next, total_q, lane);
+    mask_q<D, MT>(qc, next, lane);
     it = next;
     s_next += it.j1 - it.j0;
     if (s_next < s1) {
       const bool nr = it.g == hkv - 1;
-      next = make_item<FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
-                             nr ? it.pr + it.n : it.pr, s_next, s1);
+      next = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
+                                 nr ? it.pr + it.n : it.pr, s_next, s1);
     }
-    if constexpr (PREQ) load_q<D, MT>(qr, p, next, total_q, lane);
+    if constexpr (PREQ) load_q<D, MT>(qn, p, next, total_q, lane);
   }
 }
 
-// One dispatch of W waves (W / 4 workgroups of 4 independent waves).
+// One dispatch of W waves (W / 4 workgroups of 4 independent waves), one
+// range each.
 template <int D, int MT, bool FUSE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D * MT <= 128 ? 2 : 1)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
 void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
                              const int32_t* __restrict__ stage_table,
                              const int32_t* __restrict__ seq_lens,
                              const int32_t* __restrict__ q_indptr) {
+  constexpr int NB = span_blocks(D, MT);
   extern __shared__ uint32_t s_pre[];        // [bs + 1]: exclusive prefix of per-request spans
   __shared__ uint32_t s_wsum[4];
-  constexpr int kQBufs = D * MT <= 256 ? 2 : 1;   // one-item-ahead Q needs two buffers
-  __shared__ u32x4 s_q[4][kQBufs][MT * (D / 32) * 64];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = uniform(tid >> 6);
@@ -634,7 +705,7 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
   uint32_t carry = 0;
   for (int base = 0; base < p.bs; base += 256) {
     const int r = base + tid;
-    const uint32_t n = r < p.bs ? spans_of(clamp_len(p, seq_lens, r)) : 0;
+    const uint32_t n = r < p.bs ? spans_of<NB>(clamp_len(p, seq_lens, r)) : 0;
     uint32_t incl = n;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -660,34 +731,24 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
   if (total_q <= 0) return;   // no query rows: nothing to attend
 
   const Ranges R((int64_t)p.num_kv_heads * carry, p.num_waves);
-  const int64_t w = (int64_t)blockIdx.x * 4 + wave;
-  int64_t rid = w;
-  while (true) {
-    const int64_t b = uniform64(R.begin(rid)), e = uniform64(R.end(rid));
-    if (b < e)
-      process_range<D, MT, FUSE>(p, block_table, stage_table, seq_lens, q_indptr, s_pre,
-                                 s_q[wave][0], s_q[wave][kQBufs - 1], total_q, rid, b, e, lane);
-    uint32_t c = 0;
-    if (lane == 0)
-      c = __hip_atomic_fetch_add(p.counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    c = uniform(__shfl(c, 0));
-    if (c >= R.C) break;
-    rid = R.W + c;
-  }
+  const int64_t rid = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t b = uniform64(R.begin(rid)), e = uniform64(R.end(rid));
+  if (b < e)
+    process_range<D, MT, NB, FUSE>(p, block_table, stage_table, seq_lens, q_indptr, s_pre,
+                                   total_q, rid, b, e, lane);
 }
 
 // Merge the partials of every item that a range boundary cut, in range order
 // (deterministic, no atomics).
 template <int D, int MT>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
+  constexpr int NB = span_blocks(D, MT);
   const int g = blockIdx.x;
   const int r = blockIdx.y;
-  // the attention dispatch has finished: rewind its chunk counter for the next one
-  if (g == 0 && r == 0 && threadIdx.x == 0) *p.counters = 0;
   const int hkv = p.num_kv_heads;
   const Ranges R((int64_t)hkv * p.prefix[p.bs], p.num_waves);
   const int L = clamp_len(p, p.seq_lens, r);
-  const int n = spans_of(L);
+  const int n = spans_of<NB>(L);
   const int qo = p.q_indptr[r];
   const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
   const int64_t a = (int64_t)p.prefix[r] * hkv + (int64_t)g * n;
@@ -752,9 +813,8 @@ const void* kernel_for(int d, int mt) {
 struct Plan {
   int mt;            // 16-row tiles
   int num_waves;     // W: resident waves of the launch
-  int64_t max_chunks;
   size_t lds_bytes;  // dynamic LDS: the span prefix
-  size_t counter_bytes, prefix_bytes, trash_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
+  size_t prefix_bytes, trash_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
 };
 
 // Waves the device keeps resident for this kernel (CUs x waves per CU), or
@@ -787,18 +847,13 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool 
   if (rows > kMaxRows) return false;
   pl->mt = (rows + 15) / 16;
   pl->num_waves = resident_waves(d, pl->mt, fuse);
-  // upper bound of the dynamic chunks: at most 1 + (100-kStaticPct)% of the spans
-  const int64_t max_spans = (int64_t)hkv * bs * std::max(1, (max_seq_len + kSpan - 1) / kSpan);
-  pl->max_chunks = (max_spans - max_spans * kStaticPct / 100 + kChunkSpans - 1) / kChunkSpans + 1;
-  const size_t slots = 2 * ((size_t)pl->num_waves + (size_t)pl->max_chunks) * pl->mt * 16;
+  const size_t slots = 2 * (size_t)pl->num_waves * pl->mt * 16;
   pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t);
-  pl->counter_bytes = 256;
   pl->prefix_bytes = (((size_t)bs + 1) * sizeof(uint32_t) + 255) / 256 * 256;
   pl->trash_bytes = (size_t)2 * d * kBlock * 2;
   pl->part_o_bytes = slots * d * sizeof(float);
   pl->part_ml_bytes = slots * sizeof(float2);
-  pl->ws_bytes = pl->counter_bytes + pl->prefix_bytes + pl->trash_bytes + pl->part_o_bytes +
-                 pl->part_ml_bytes;
+  pl->ws_bytes = pl->prefix_bytes + pl->trash_bytes + pl->part_o_bytes + pl->part_ml_bytes;
   return true;
 }
 
@@ -847,6 +902,9 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
     return fail(NSD_ERR_SHAPE, "%s: max_seq_len, max_blocks_per_seq and num_blocks must be "
                 ">= 1", fn);
   if (fuse && stage_blocks < 0) return fail(NSD_ERR_SHAPE, "%s: stage_num_blocks < 0", fn);
+  // tiles (block, KV head) are indexed with 32-bit integers
+  if (num_blocks > INT32_MAX / num_kv_heads || (fuse && stage_blocks > INT32_MAX / num_kv_heads))
+    return fail(NSD_ERR_UNSUPPORTED, "%s: more than 2^31-1 (block, KV head) tiles in a pool", fn);
   if (!(scale == scale) || isinf(scale)) return fail(NSD_ERR_SHAPE, "%s: scale must be finite", fn);
   if (bs == 0) return NSD_OK;
   if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !q_indptr || !out ||
@@ -883,14 +941,12 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   p.q_indptr = q_indptr;
   p.out = (uint16_t*)out;
   char* ws = (char*)workspace;
-  p.counters = (uint32_t*)ws;
-  p.prefix = (uint32_t*)(ws + pl.counter_bytes);
-  p.trash = (uint16_t*)(ws + pl.counter_bytes + pl.prefix_bytes);
-  p.part_o = (float*)(ws + pl.counter_bytes + pl.prefix_bytes + pl.trash_bytes);
-  p.part_ml = (float2*)(ws + pl.counter_bytes + pl.prefix_bytes + pl.trash_bytes +
-                        pl.part_o_bytes);
-  p.num_blocks = num_blocks;
-  p.stage_blocks = fuse ? stage_blocks : 0;
+  p.prefix = (uint32_t*)ws;
+  p.trash = (uint16_t*)(ws + pl.prefix_bytes);
+  p.part_o = (float*)(ws + pl.prefix_bytes + pl.trash_bytes);
+  p.part_ml = (float2*)(ws + pl.prefix_bytes + pl.trash_bytes + pl.part_o_bytes);
+  p.num_blocks = (int32_t)num_blocks;
+  p.stage_blocks = fuse ? (int32_t)stage_blocks : 0;
   p.bs = bs;
   p.max_blocks_per_seq = max_blocks_per_seq;
   p.num_q_heads = num_q_heads;
