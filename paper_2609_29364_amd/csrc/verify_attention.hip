@@ -97,6 +97,7 @@ struct Params {
   int32_t max_q;
   int32_t max_seq_len;
   int32_t num_waves;
+  int32_t w_even, w_odd;   // relative range lengths of waves on even / odd XCDs
   float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -177,34 +178,68 @@ __device__ inline int spans_of(int L) {
   return max(1, (L + NB * kBlock - 1) / (NB * kBlock));
 }
 
-// One (request r, KV head g) item restricted to spans [j0, j1) of a range.
+// Work units of one span in the stream-K split.  In the fused variant a span
+// of an arriving request also writes its tiles to the worker pool, which costs
+// HBM time beside the read; the split weighs it accordingly.
+constexpr int kResidentCost = 4;
+constexpr int kArrivingCost = 6;
+
+__device__ inline bool is_arriving(const Params& p, const int32_t* __restrict__ stage_table,
+                                   int r) {
+  return p.stage_blocks > 0 && stage_table[(int64_t)r * p.max_blocks_per_seq] >= 0;
+}
+
+__device__ inline int ceil_div_pos(int64_t a, int c) { return a <= 0 ? 0 : (int)((a + c - 1) / c); }
+
+// Spans of an item (n spans of c units from unit position base) whose start
+// lies in [b, e).
+__device__ inline void spans_in(int64_t base, int c, int n, int64_t b, int64_t e, int& j0,
+                                int& j1) {
+  j0 = min(n, ceil_div_pos(b - base, c));
+  j1 = min(n, ceil_div_pos(e - base, c));
+}
+
+// One (request r, KV head g) item restricted to the spans [j0, j1) whose
+// start lies in a range.
 struct Item {
-  int r, g, L, n, qo, nq, rows, win, j0, j1;
-  int64_t pr;        // exclusive span prefix of request r (per KV head)
+  int r, g, L, n, c, qo, nq, rows, win, j0, j1;
+  int64_t pr;        // exclusive unit prefix of request r (per KV head)
+  int64_t base;      // unit position of the item's first span
   bool arriving;     // fused variant: K/V come from the staging pool
 };
 
 template <int NB, bool FUSE>
 __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
-                                 const int32_t* __restrict__ stage_table, int r, int64_t pr,
-                                 int64_t s, int64_t s1) {
+                                 const int32_t* __restrict__ stage_table, int r, int g,
+                                 int64_t pr, int64_t s, int64_t s1) {
   Item it;
   it.r = r;
+  it.g = g;
   it.pr = pr;
   it.L = clamp_len(p, seq_lens, r);
   it.n = spans_of<NB>(it.L);
+  it.arriving = FUSE && is_arriving(p, stage_table, r);
+  it.c = it.arriving ? kArrivingCost : kResidentCost;
+  it.base = (int64_t)p.num_kv_heads * pr + (int64_t)g * it.n * it.c;
+  spans_in(it.base, it.c, it.n, s, s1, it.j0, it.j1);
   it.qo = q_indptr[r];
   it.nq = max(0, min(q_indptr[r + 1] - it.qo, p.max_q));
-  const int64_t off = s - (int64_t)p.num_kv_heads * pr;
-  it.g = (int)(off / it.n);
-  it.j0 = (int)(off - (int64_t)it.g * it.n);
-  it.j1 = (int)min((int64_t)it.n, it.j0 + (s1 - s));
   it.rows = p.group * it.nq;
   it.win = it.L - it.nq;
-  it.arriving = FUSE && p.stage_blocks > 0 &&
-                stage_table[(int64_t)r * p.max_blocks_per_seq] >= 0;
   return it;
+}
+
+// The item after `it` in (request, KV head) order.
+template <int NB, bool FUSE>
+__device__ inline Item next_item(const Params& p, const int32_t* __restrict__ seq_lens,
+                                 const int32_t* __restrict__ q_indptr,
+                                 const int32_t* __restrict__ stage_table, const Item& it,
+                                 int64_t s, int64_t s1) {
+  const bool nr = it.g == p.num_kv_heads - 1;
+  return make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
+                             nr ? 0 : it.g + 1, nr ? it.pr + (int64_t)it.n * it.c : it.pr, s,
+                             s1);
 }
 
 // Raw block-table entries of one span (scalar loads, checked later).
@@ -570,16 +605,35 @@ __device__ inline void finish_item(const Params& p, Acc<D, MT>& a, const Item& i
   }
 }
 
-// The global sequence of T spans (ordered by request, then KV head, then
-// position) is cut into W equal contiguous ranges, one per resident wave.
-// Every kernel derives the same ranges from T and W.
+// The global sequence of T work units (spans in request, KV head, position
+// order, each span weighing its unit cost) is cut into W contiguous ranges,
+// one per resident wave, sized by the wave's speed: workgroups are dealt to
+// the eight XCDs in turn, and waves on odd XCDs stream HBM measurably slower
+// than those on even ones, so their ranges are shorter in the ratio
+// w_odd : w_even.  Every kernel derives the same ranges from T, W and the
+// weights.
 struct Ranges {
-  int64_t T, W;
-  __device__ Ranges(int64_t total, int64_t waves) : T(total), W(waves) {}
-  __device__ int64_t begin(int64_t rid) const { return rid * T / W; }
-  __device__ int64_t end(int64_t rid) const { return (rid + 1) * T / W; }
-  // range holding span s
-  __device__ int64_t of(int64_t s) const { return ((s + 1) * W - 1) / T; }
+  int64_t T, W, we, wo, total;
+  __device__ Ranges(int64_t t, int64_t waves, int w_even, int w_odd)
+      : T(t), W(waves), we(w_even), wo(w_odd) {
+    total = weight_before(W);
+  }
+  // summed weight of ranges [0, q): range q is wave q % 4 of workgroup q / 4
+  __device__ int64_t weight_before(int64_t q) const {
+    const int64_t k = q % 8;
+    return (q / 8) * 4 * (we + wo) + (k < 4 ? k * we : 4 * we + (k - 4) * wo);
+  }
+  __device__ int64_t begin(int64_t rid) const { return T * weight_before(rid) / total; }
+  __device__ int64_t end(int64_t rid) const { return T * weight_before(rid + 1) / total; }
+  // range holding unit s (the last range whose begin is <= s)
+  __device__ int64_t of(int64_t s) const {
+    int64_t lo = 0, hi = W - 1;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (begin(mid) <= s) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+  }
 };
 
 // Request whose spans [hkv*pre[r], hkv*pre[r+1]) contain global span s.
@@ -636,15 +690,26 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
                               int64_t s1, int lane) {
   const int hkv = p.num_kv_heads;
   const int r0 = uniform(find_request(pre, p.bs, hkv, s));
-  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, r0, uniform64(pre[r0]), s,
-                                s1);
-  Item next = it;
-  int64_t s_next = s + (it.j1 - it.j0);
-  if (s_next < s1) {
-    const bool nr = it.g == hkv - 1;
-    next = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
-                               nr ? it.pr + it.n : it.pr, s_next, s1);
+  const int64_t pr0 = uniform64(pre[r0]);
+  // the item holding unit position s; it is empty here when s falls inside
+  // its last span (that span belongs to the range where it starts)
+  const int nc0 = spans_of<NB>(clamp_len(p, seq_lens, r0)) *
+                  (FUSE && is_arriving(p, stage_table, r0) ? kArrivingCost : kResidentCost);
+  const int g0 = (int)min((int64_t)hkv - 1, (s - (int64_t)hkv * pr0) / nc0);
+  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, r0, g0, pr0, s, s1);
+  if (it.j0 >= it.j1) {
+    if (it.r == p.bs - 1 && it.g == hkv - 1) return;
+    it = next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, it, s, s1);
+    if (it.j0 >= it.j1) return;   // no span starts in this range
   }
+  // next item with a span starting in the range (or `it` itself when none)
+  auto following = [&](const Item& cur) {
+    const bool last = cur.r == p.bs - 1 && cur.g == hkv - 1;
+    if (last || cur.base + (int64_t)cur.n * cur.c >= s1) return cur;
+    return next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, cur, s, s1);
+  };
+  Item next = following(it);
+  bool more = next.base != it.base;
 
   // Q of the next item is fetched one item ahead when the tile leaves room
   // for a second copy (PREQ); larger tiles fetch it at the switch.
@@ -669,18 +734,14 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
       run_item<D, MT, NB, FUSE, false>(p, block_table, stage_table, it, next, kreg, vreg, cur,
                                        qc, a, lane);
     finish_item<D, MT>(p, a, it, rid, lane);
-    if (s_next >= s1) break;
+    if (!more) break;
     // switch to the next item
     if constexpr (PREQ) qc = qn;
     else load_q<D, MT>(qc, p, next, total_q, lane);
     mask_q<D, MT>(qc, next, lane);
     it = next;
-    s_next += it.j1 - it.j0;
-    if (s_next < s1) {
-      const bool nr = it.g == hkv - 1;
-      next = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
-                                 nr ? it.pr + it.n : it.pr, s_next, s1);
-    }
+    next = following(it);
+    more = next.base != it.base;
     if constexpr (PREQ) load_q<D, MT>(qn, p, next, total_q, lane);
   }
 }
@@ -701,11 +762,15 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
   const int wave = uniform(tid >> 6);
   const int total_q = uniform(q_indptr[p.bs]);
 
-  // prefix of per-request span counts (every workgroup keeps its own copy)
+  // prefix of per-request work units (spans times their unit cost); every
+  // workgroup keeps its own copy
   uint32_t carry = 0;
   for (int base = 0; base < p.bs; base += 256) {
     const int r = base + tid;
-    const uint32_t n = r < p.bs ? spans_of<NB>(clamp_len(p, seq_lens, r)) : 0;
+    const uint32_t n =
+        r < p.bs ? spans_of<NB>(clamp_len(p, seq_lens, r)) *
+                       (FUSE && is_arriving(p, stage_table, r) ? kArrivingCost : kResidentCost)
+                 : 0;
     uint32_t incl = n;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -730,7 +795,7 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
   __syncthreads();
   if (total_q <= 0) return;   // no query rows: nothing to attend
 
-  const Ranges R((int64_t)p.num_kv_heads * carry, p.num_waves);
+  const Ranges R((int64_t)p.num_kv_heads * carry, p.num_waves, p.w_even, p.w_odd);
   const int64_t rid = (int64_t)blockIdx.x * 4 + wave;
   const int64_t b = uniform64(R.begin(rid)), e = uniform64(R.end(rid));
   if (b < e)
@@ -746,14 +811,15 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const int g = blockIdx.x;
   const int r = blockIdx.y;
   const int hkv = p.num_kv_heads;
-  const Ranges R((int64_t)hkv * p.prefix[p.bs], p.num_waves);
+  const Ranges R((int64_t)hkv * p.prefix[p.bs], p.num_waves, p.w_even, p.w_odd);
   const int L = clamp_len(p, p.seq_lens, r);
   const int n = spans_of<NB>(L);
+  const int c = is_arriving(p, p.stage_table, r) ? kArrivingCost : kResidentCost;
   const int qo = p.q_indptr[r];
   const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
-  const int64_t a = (int64_t)p.prefix[r] * hkv + (int64_t)g * n;
-  const int64_t ra = R.of(a);
-  const int64_t rb = R.of(a + n - 1);
+  const int64_t base = (int64_t)p.prefix[r] * hkv + (int64_t)g * n * c;
+  const int64_t ra = R.of(base);                          // range of the first span's start
+  const int64_t rb = R.of(base + (int64_t)(n - 1) * c);   // range of the last span's start
   if (ra == rb || nq == 0) return;
   const int rows = p.group * nq;
   constexpr int kVec = D / 4;
@@ -762,15 +828,19 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
     const int d = (idx % kVec) * 4;
     float mx = -INFINITY;
     for (int64_t q = ra; q <= rb; ++q) {
-      if (R.begin(q) >= R.end(q)) continue;
-      const int64_t slot = 2 * q + (q == ra ? 1 : 0);
+      int j0, j1;
+      spans_in(base, c, n, R.begin(q), R.end(q), j0, j1);
+      if (j0 >= j1) continue;   // no span of the item starts in range q
+      const int64_t slot = 2 * q + (j0 > 0 ? 0 : 1);
       mx = fmaxf(mx, p.part_ml[slot * (MT * 16) + m].x);
     }
     f32x4 num = {0.f, 0.f, 0.f, 0.f};
     float den = 0.f;
     for (int64_t q = ra; q <= rb; ++q) {
-      if (R.begin(q) >= R.end(q)) continue;
-      const int64_t slot = 2 * q + (q == ra ? 1 : 0);
+      int j0, j1;
+      spans_in(base, c, n, R.begin(q), R.end(q), j0, j1);
+      if (j0 >= j1) continue;
+      const int64_t slot = 2 * q + (j0 > 0 ? 0 : 1);
       const float2 ml = p.part_ml[slot * (MT * 16) + m];
       const float wt = (ml.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml.x - mx);
       const f32x4 o = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
@@ -955,6 +1025,10 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   p.max_q = max_q_per_seq;
   p.max_seq_len = max_seq_len;
   p.num_waves = pl.num_waves;
+  // measured HBM streaming speed of odd-XCD waves relative to even ones (the
+  // fused pass also writes, which widens the gap)
+  p.w_even = 100;
+  p.w_odd = fuse ? 91 : 94;
   p.scale_log2 = scale * 1.4426950408889634f;
 
   clear_stale_error();
