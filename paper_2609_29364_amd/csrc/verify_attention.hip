@@ -625,14 +625,16 @@ struct Ranges {
   }
   __device__ int64_t begin(int64_t rid) const { return T * weight_before(rid) / total; }
   __device__ int64_t end(int64_t rid) const { return T * weight_before(rid + 1) / total; }
-  // range holding unit s (the last range whose begin is <= s)
+  // range holding unit s: the last q with begin(q) <= s, i.e. the last q
+  // with weight_before(q) <= G = floor(((s + 1) * total - 1) / T), found by
+  // inverting the piecewise-linear weight_before
   __device__ int64_t of(int64_t s) const {
-    int64_t lo = 0, hi = W - 1;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (begin(mid) <= s) lo = mid; else hi = mid - 1;
-    }
-    return lo;
+    const int64_t G = ((s + 1) * total - 1) / T;
+    const int64_t blk = 4 * (we + wo);
+    const int64_t full = G / blk;
+    const int64_t rem = G - full * blk;
+    const int64_t k = rem < 4 * we ? rem / we : 4 + min((int64_t)3, (rem - 4 * we) / wo);
+    return min(W - 1, full * 8 + k);
   }
 };
 
@@ -804,13 +806,17 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
 }
 
 // Merge the partials of every item that a range boundary cut, in range order
-// (deterministic, no atomics).
+// (deterministic, no atomics).  One workgroup per (KV head, request); the
+// ranges holding the item's spans and their partial slots are found once per
+// workgroup.
 template <int D, int MT>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   constexpr int NB = span_blocks(D, MT);
+  __shared__ int64_t s_slot[256];   // partial slots of the item, in range order
   const int g = blockIdx.x;
   const int r = blockIdx.y;
   const int hkv = p.num_kv_heads;
+  const int tid = threadIdx.x;
   const Ranges R((int64_t)hkv * p.prefix[p.bs], p.num_waves, p.w_even, p.w_odd);
   const int L = clamp_len(p, p.seq_lens, r);
   const int n = spans_of<NB>(L);
@@ -818,41 +824,70 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const int qo = p.q_indptr[r];
   const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
   const int64_t base = (int64_t)p.prefix[r] * hkv + (int64_t)g * n * c;
-  const int64_t ra = R.of(base);                          // range of the first span's start
-  const int64_t rb = R.of(base + (int64_t)(n - 1) * c);   // range of the last span's start
+  const int64_t ra = uniform64(R.of(base));                          // first span's range
+  const int64_t rb = uniform64(R.of(base + (int64_t)(n - 1) * c));   // last span's range
   if (ra == rb || nq == 0) return;
   const int rows = p.group * nq;
   constexpr int kVec = D / 4;
-  for (int idx = threadIdx.x; idx < rows * kVec; idx += blockDim.x) {
+  // running merge over the ranges, 256 at a time (an item rarely spans more
+  // than a few)
+  constexpr int kPer = (kMaxRows * kVec + 255) / 256;   // elements per thread
+  float mrun[kPer], drun[kPer];
+  f32x4 orun[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    mrun[i] = -INFINITY;
+    drun[i] = 0.f;
+    orun[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int64_t q0 = ra; q0 <= rb; q0 += 256) {
+    const int64_t q = q0 + tid;
+    if (q <= rb) {
+      int j0, j1;
+      spans_in(base, c, n, R.begin(q), R.end(q), j0, j1);
+      if (j0 < j1) {
+        // ranges are visited in order below, so keep the order: compact by rank
+        s_slot[tid] = 2 * q + (j0 > 0 ? 0 : 1);
+      } else {
+        s_slot[tid] = -1;
+      }
+    }
+    const int cnt = (int)min((int64_t)256, rb - q0 + 1);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int idx = tid + i * 256;
+      if (idx >= rows * kVec) break;
+      const int m = idx / kVec;
+      const int d = (idx % kVec) * 4;
+      for (int k = 0; k < cnt; ++k) {
+        const int64_t slot = s_slot[k];
+        if (slot < 0) continue;   // no span of the item starts in that range
+        const float2 ml = p.part_ml[slot * (MT * 16) + m];
+        if (ml.x == -INFINITY) continue;
+        const f32x4 o = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
+        const float mx = fmaxf(mrun[i], ml.x);
+        const float a = mrun[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun[i] - mx);
+        const float b = __builtin_amdgcn_exp2f(ml.x - mx);
+        orun[i] = a * orun[i] + b * o;
+        drun[i] = a * drun[i] + b * ml.y;
+        mrun[i] = mx;
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int idx = tid + i * 256;
+    if (idx >= rows * kVec) break;
     const int m = idx / kVec;
     const int d = (idx % kVec) * 4;
-    float mx = -INFINITY;
-    for (int64_t q = ra; q <= rb; ++q) {
-      int j0, j1;
-      spans_in(base, c, n, R.begin(q), R.end(q), j0, j1);
-      if (j0 >= j1) continue;   // no span of the item starts in range q
-      const int64_t slot = 2 * q + (j0 > 0 ? 0 : 1);
-      mx = fmaxf(mx, p.part_ml[slot * (MT * 16) + m].x);
-    }
-    f32x4 num = {0.f, 0.f, 0.f, 0.f};
-    float den = 0.f;
-    for (int64_t q = ra; q <= rb; ++q) {
-      int j0, j1;
-      spans_in(base, c, n, R.begin(q), R.end(q), j0, j1);
-      if (j0 >= j1) continue;
-      const int64_t slot = 2 * q + (j0 > 0 ? 0 : 1);
-      const float2 ml = p.part_ml[slot * (MT * 16) + m];
-      const float wt = (ml.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml.x - mx);
-      const f32x4 o = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
-      num += wt * o;
-      den += wt * ml.y;
-    }
-    const float inv = den > 0.f ? 1.f / den : 0.f;
+    const float inv = drun[i] > 0.f ? 1.f / drun[i] : 0.f;
     const int j = m / p.group;
     const int h = g * p.group + m % p.group;
     uint16_t* dst = p.out + ((int64_t)(qo + j) * p.num_q_heads + h) * D + d;
-    const bf16x2 lo = {(__bf16)(num[0] * inv), (__bf16)(num[1] * inv)};
-    const bf16x2 hi = {(__bf16)(num[2] * inv), (__bf16)(num[3] * inv)};
+    const bf16x2 lo = {(__bf16)(orun[i][0] * inv), (__bf16)(orun[i][1] * inv)};
+    const bf16x2 hi = {(__bf16)(orun[i][2] * inv), (__bf16)(orun[i][3] * inv)};
     *(u32x2*)dst = u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
   }
 }
