@@ -86,7 +86,6 @@ struct Params {
   float* part_o;       // [2 * ranges][MT*16][D]: head/tail partial O per range
   float2* part_ml;     // [2 * ranges][MT*16]: (running max, sum)
   uint32_t* prefix;    // [bs+1]: exclusive prefix of per-request span counts
-  uint16_t* trash;     // one K tile + one V tile that absorb stores to invalid ids
   int32_t num_blocks;    // blocks in the worker pool (tiles fit 32-bit indexes)
   int32_t stage_blocks;  // blocks in the staging pool (0 without fusion)
   int32_t bs;
@@ -254,7 +253,7 @@ struct SpanRef {
   const uint16_t* k_src;  // planes the span is read from (pool or staging)
   const uint16_t* v_src;
   int32_t ts[NB];         // source tiles (block * num_kv_heads + head)
-  int32_t td[NB];         // destination tiles (fused); -1: the trash tiles
+  int32_t td[NB];         // destination tiles (fused); -1: not written
   int32_t t;              // first token of the span
   uint32_t bad;           // bit b: block b's id is out of range (its tokens are invisible)
 };
@@ -281,8 +280,8 @@ __device__ inline SpanIds<NB> load_ids(const Params& p, const int32_t* __restric
 }
 
 // Span j of item it from its table entries.  Blocks past the context reuse
-// block 0's tile (their tokens are masked) and send fused stores to the trash
-// tiles, as do arriving blocks with an invalid staging or destination id.
+// block 0's tile (their tokens are masked) and are not written by the fused
+// variant, nor are arriving blocks with an invalid staging or destination id.
 template <int NB, bool FUSE>
 __device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
                                        const SpanIds<NB>& ids) {
@@ -345,7 +344,8 @@ __device__ inline void store_k(const KOps<D, NB>& o, const Params& p, const Span
   const int row = lane & 15, grp = lane >> 4;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    uint16_t* dst = s.td[b] >= 0 ? p.k_dst + (int64_t)s.td[b] * (D * kBlock) : p.trash;
+    if (s.td[b] < 0) continue;   // block past the context, or an invalid id
+    uint16_t* dst = p.k_dst + (int64_t)s.td[b] * (D * kBlock);
 #pragma unroll
     for (int kk = 0; kk < D / 32; ++kk) {
       const int off = ((kk * 4 + grp) * kBlock + row) * 8;
@@ -360,8 +360,8 @@ __device__ inline void store_v(const VOps<D, NB>& o, const Params& p, const Span
   const int row = lane & 15, grp = lane >> 4;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    uint16_t* dst =
-        s.td[b] >= 0 ? p.v_dst + (int64_t)s.td[b] * (D * kBlock) : p.trash + D * kBlock;
+    if (s.td[b] < 0) continue;
+    uint16_t* dst = p.v_dst + (int64_t)s.td[b] * (D * kBlock);
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) {
       const int off = (dt * 16 + row) * kBlock + grp * 4;
@@ -919,7 +919,7 @@ struct Plan {
   int mt;            // 16-row tiles
   int num_waves;     // W: resident waves of the launch
   size_t lds_bytes;  // dynamic LDS: the span prefix
-  size_t prefix_bytes, trash_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
+  size_t prefix_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
 };
 
 // Waves the device keeps resident for this kernel (CUs x waves per CU), or
@@ -955,10 +955,9 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool 
   const size_t slots = 2 * (size_t)pl->num_waves * pl->mt * 16;
   pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t);
   pl->prefix_bytes = (((size_t)bs + 1) * sizeof(uint32_t) + 255) / 256 * 256;
-  pl->trash_bytes = (size_t)2 * d * kBlock * 2;
   pl->part_o_bytes = slots * d * sizeof(float);
   pl->part_ml_bytes = slots * sizeof(float2);
-  pl->ws_bytes = pl->prefix_bytes + pl->trash_bytes + pl->part_o_bytes + pl->part_ml_bytes;
+  pl->ws_bytes = pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes;
   return true;
 }
 
@@ -1047,9 +1046,8 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   p.out = (uint16_t*)out;
   char* ws = (char*)workspace;
   p.prefix = (uint32_t*)ws;
-  p.trash = (uint16_t*)(ws + pl.prefix_bytes);
-  p.part_o = (float*)(ws + pl.prefix_bytes + pl.trash_bytes);
-  p.part_ml = (float2*)(ws + pl.prefix_bytes + pl.trash_bytes + pl.part_o_bytes);
+  p.part_o = (float*)(ws + pl.prefix_bytes);
+  p.part_ml = (float2*)(ws + pl.prefix_bytes + pl.part_o_bytes);
   p.num_blocks = (int32_t)num_blocks;
   p.stage_blocks = fuse ? (int32_t)stage_blocks : 0;
   p.bs = bs;

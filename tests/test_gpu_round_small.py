@@ -31,20 +31,12 @@ def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None, fused=False
     if waves:
         os.environ["NSD_ATTN_WAVES"] = str(waves)
     try:
-        if fused:
-            bt, st = i32(meta.block_table, dev), i32(meta.stage_table, dev)
-            sl, qi = i32(meta.seq_lens, dev), i32(meta.q_indptr, dev)
-            outs = [nsd.gather_verify_attention(q[l], kp[l], vp[l], ks[l], vs[l], bt, st, sl, qi,
-                                                meta.max_q, meta.max_seq_len)
-                    for l in range(cfg.num_layers)]
-            acc = tok = None
-            if acc_dev is not None:
-                acc, tok = nsd.spec_accept(*acc_dev[:4], qi, acc_dev[4])
-        else:
-            outs, acc, tok = verify_round(kp, vp, ks, vs, i32(meta.src_ids, dev),
-                                          i32(meta.dst_ids, dev), q, i32(meta.block_table, dev),
-                                          i32(meta.seq_lens, dev), i32(meta.q_indptr, dev),
-                                          meta.max_q, meta.max_seq_len, accept=acc_dev)
+        st = i32(meta.stage_table, dev) if fused else None
+        outs, acc, tok = verify_round(kp, vp, ks, vs, i32(meta.src_ids, dev),
+                                      i32(meta.dst_ids, dev), q, i32(meta.block_table, dev),
+                                      i32(meta.seq_lens, dev), i32(meta.q_indptr, dev),
+                                      meta.max_q, meta.max_seq_len, accept=acc_dev,
+                                      stage_table=st)
         torch.cuda.synchronize()
     finally:
         if waves:
@@ -199,6 +191,44 @@ def test_out_of_range_block_ids_are_invisible(device):
                                                     v[:48].double().numpy(), 0.125)
     # the oracle places the query at the last visible position, which is the same set of keys
     assert np.abs(out[1:2].float().cpu().numpy() - ref).max() <= 2e-2
+
+
+def test_fused_out_of_range_ids(device):
+    # fused pass: a staging id past the staging pool hides its tokens and leaves the
+    # destination unwritten; a destination id past the pool is not written, while its
+    # (valid) staged tokens stay visible
+    cfg = custom_config(seed=32, bs=2, vocab=0, n_arriving=2, ctx_lo=64, ctx_hi=64, k_lo=0,
+                        k_hi=0, pool_blocks=None)
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    st = meta.stage_table.copy()
+    bt = meta.block_table.copy()
+    st[1, 3] = meta.stage_num_blocks + 100   # request 1: tokens 48..63 vanish, block not written
+    bt[0, 2] = meta.num_blocks + 5           # request 0: block 2 not written, still attended
+    kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
+    out = nsd.gather_verify_attention(lay.q.to(device), kp, vp, lay.k_stage.to(device),
+                                      lay.v_stage.to(device), i32(bt, device), i32(st, device),
+                                      i32(meta.seq_lens, device), i32(meta.q_indptr, device), 1, 64)
+    torch.cuda.synchronize()
+    # pool: the pairs that stayed valid are copied, the two dropped blocks keep their bytes
+    keep = [(int(meta.stage_table[r, b]), int(meta.block_table[r, b]))
+            for r in range(2) for b in range(4) if (r, b) not in ((1, 3), (0, 2))]
+    ref_k, ref_v = oracle.gather.kv_gather(u16(lay.k_stage)[None], u16(lay.v_stage)[None],
+                                           u16(lay.k_pool)[None], u16(lay.v_pool)[None],
+                                           np.array([a for a, _ in keep]),
+                                           np.array([b for _, b in keep]))
+    assert np.array_equal(u16(kp.cpu()), ref_k[0]) and np.array_equal(u16(vp.cpu()), ref_v[0])
+    from workload.synth import logical_kv
+    qs = lay.q.double().numpy()
+    k0, v0 = logical_kv(meta, lay, 0)
+    ref0 = oracle.attention.verify_attention_request(qs[0:1], k0.double().numpy(),
+                                                     v0.double().numpy(), 0.125)
+    k1, v1 = logical_kv(meta, lay, 1)
+    ref1 = oracle.attention.verify_attention_request(qs[1:2], k1[:48].double().numpy(),
+                                                     v1[:48].double().numpy(), 0.125)
+    got = out.float().cpu().numpy()
+    assert np.abs(got[0:1] - ref0).max() <= 2e-2
+    assert np.abs(got[1:2] - ref1).max() <= 2e-2
 
 
 # ---------------------------------------------------------------- acceptance
