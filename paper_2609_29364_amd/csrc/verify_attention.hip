@@ -813,6 +813,7 @@ template <int D, int MT>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   constexpr int NB = span_blocks(D, MT);
   __shared__ int64_t s_slot[256];   // partial slots of the item, in range order
+  __shared__ int s_nslot;
   const int g = blockIdx.x;
   const int r = blockIdx.y;
   const int hkv = p.num_kv_heads;
@@ -845,33 +846,44 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
     if (q <= rb) {
       int j0, j1;
       spans_in(base, c, n, R.begin(q), R.end(q), j0, j1);
-      if (j0 < j1) {
-        // ranges are visited in order below, so keep the order: compact by rank
-        s_slot[tid] = 2 * q + (j0 > 0 ? 0 : 1);
-      } else {
-        s_slot[tid] = -1;
-      }
+      s_slot[tid] = j0 < j1 ? 2 * q + (j0 > 0 ? 0 : 1) : -1;
     }
-    const int cnt = (int)min((int64_t)256, rb - q0 + 1);
     __syncthreads();
+    if (tid == 0) {   // keep the ranges holding a part, in order
+      const int span = (int)min((int64_t)256, rb - q0 + 1);
+      int n = 0;
+      for (int k = 0; k < span; ++k)
+        if (s_slot[k] >= 0) s_slot[n++] = s_slot[k];
+      s_nslot = n;
+    }
+    __syncthreads();
+    const int cnt = s_nslot;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int idx = tid + i * 256;
       if (idx >= rows * kVec) break;
       const int m = idx / kVec;
       const int d = (idx % kVec) * 4;
-      for (int k = 0; k < cnt; ++k) {
-        const int64_t slot = s_slot[k];
-        if (slot < 0) continue;   // no span of the item starts in that range
-        const float2 ml = p.part_ml[slot * (MT * 16) + m];
-        if (ml.x == -INFINITY) continue;
-        const f32x4 o = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
-        const float mx = fmaxf(mrun[i], ml.x);
-        const float a = mrun[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun[i] - mx);
-        const float b = __builtin_amdgcn_exp2f(ml.x - mx);
-        orun[i] = a * orun[i] + b * o;
-        drun[i] = a * drun[i] + b * ml.y;
-        mrun[i] = mx;
+      // two parts at a time: both parts' loads are issued before their merge
+      for (int k0 = 0; k0 < cnt; k0 += 2) {
+        float2 ml[2];
+        f32x4 o[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int64_t slot = s_slot[min(k0 + u, cnt - 1)];
+          ml[u] = p.part_ml[slot * (MT * 16) + m];
+          o[u] = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          if (k0 + u >= cnt || ml[u].x == -INFINITY) continue;   // no visible token there
+          const float mx = fmaxf(mrun[i], ml[u].x);
+          const float a = mrun[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun[i] - mx);
+          const float b = __builtin_amdgcn_exp2f(ml[u].x - mx);
+          orun[i] = a * orun[i] + b * o[u];
+          drun[i] = a * drun[i] + b * ml[u].y;
+          mrun[i] = mx;
+        }
       }
     }
     __syncthreads();

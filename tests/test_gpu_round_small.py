@@ -170,6 +170,52 @@ def test_attention_deterministic_and_permutation_invariant(device):
     check_attention(meta, lay, o1, range(cfg.bs))
 
 
+@pytest.mark.parametrize("waves", [None, 8])
+def test_workspace_reuse(device, waves):
+    # calls that reuse one workspace (split partials of the previous call still in it),
+    # alternating the fused and unfused entry points, agree bit for bit
+    cfg = custom_config(seed=22, bs=5, num_q_heads=16, num_kv_heads=4, head_dim=128, vocab=0,
+                        ctx_lo=300, ctx_hi=1200, k_lo=2, k_hi=2, n_arriving=2, pool_blocks=None)
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    old = os.environ.get("NSD_ATTN_WAVES")
+    if waves:
+        os.environ["NSD_ATTN_WAVES"] = str(waves)
+    try:
+        n = nsd.verify_attention_workspace_size(cfg.bs, cfg.num_q_heads, cfg.num_kv_heads,
+                                                cfg.head_dim, meta.max_q, meta.max_seq_len)
+        ws = nsd.new_workspace(n, device)
+        q = lay.q.to(device)
+        sl, qi, bt = (i32(meta.seq_lens, device), i32(meta.q_indptr, device),
+                      i32(meta.block_table, device))
+        kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
+        outs = []
+        for fused in (False, True, True, False):
+            k2, v2 = kp.clone(), vp.clone()
+            if fused:
+                o = nsd.gather_verify_attention(q, k2, v2, lay.k_stage.to(device),
+                                                lay.v_stage.to(device), bt,
+                                                i32(meta.stage_table, device), sl, qi,
+                                                meta.max_q, meta.max_seq_len, workspace=ws)
+            else:
+                nsd.kv_gather(lay.k_stage.to(device), lay.v_stage.to(device), k2, v2,
+                              i32(meta.src_ids, device), i32(meta.dst_ids, device))
+                o = nsd.verify_attention(q, k2, v2, bt, sl, qi, meta.max_q, meta.max_seq_len,
+                                         workspace=ws)
+            torch.cuda.synchronize()
+            outs.append(o.clone())
+    finally:
+        if waves:
+            if old is None:
+                del os.environ["NSD_ATTN_WAVES"]
+            else:
+                os.environ["NSD_ATTN_WAVES"] = old
+    assert torch.equal(outs[1].view(torch.int16), outs[2].view(torch.int16))
+    assert torch.equal(outs[0].view(torch.int16), outs[3].view(torch.int16))
+    for o in outs:
+        check_attention(meta, lay, o, range(cfg.bs))
+
+
 def test_out_of_range_block_ids_are_invisible(device):
     # a block id past the pool makes its tokens invisible; nothing faults
     cfg = custom_config(seed=31, bs=2, vocab=0, n_arriving=0, ctx_lo=64, ctx_hi=64, k_lo=0, k_hi=0,
