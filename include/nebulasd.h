@@ -10,7 +10,8 @@
  *   nsd_spec_accept       acceptance of proposals and residual resampling
  *
  * nsd_gather_verify_attention does the first two in one pass (each staged
- * byte read once).
+ * byte read once); nsd_copy_plan moves KV between a pinned host arena and a
+ * device bank (the host-side source of the preparation).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -191,6 +192,35 @@ nsd_status nsd_gather_verify_attention(const void* q, void* k_cache, void* v_cac
                                        int32_t max_q_per_seq, int32_t max_seq_len, float scale,
                                        void* out, void* workspace, size_t workspace_bytes,
                                        void* stream);
+
+#define NSD_COPY_H2D 1  /* pinned host -> device */
+#define NSD_COPY_D2H 2  /* device -> pinned host */
+
+/*
+ * Execute a KV copy plan between a pinned host arena (HostKV) and device
+ * memory (a KV bank) on the DMA engines, asynchronously on `stream`.
+ *
+ * Passage: Appendix E.1 (persistent host KV arenas addressed by numeric
+ * offsets; each request owns a stable extent of blocks, Eq. E.1), Appendix
+ * E.4 (copy plans as compact descriptors), Appendix E.5 (H2D plans are
+ * split into bounded chunks, 32 MiB by default).
+ *
+ * copies : host, int64 [n_copies][3] = (source byte offset, destination byte
+ *          offset, bytes).  Each triple must lie inside [0, src_bytes) and
+ *          [0, dst_bytes).  Triples that continue the previous one in both
+ *          buffers are merged; every run is issued as copies of at most
+ *          chunk_bytes (>= 1) bytes, in plan order.
+ * direction : NSD_COPY_H2D (src pinned host, dst device) or NSD_COPY_D2H
+ *          (src device, dst pinned host).  The host side must be pinned
+ *          memory (hipHostMalloc; registering existing pages is not used),
+ *          else NSD_ERR_UNSUPPORTED.
+ * Overlapping destination ranges give unspecified bytes.  n_copies == 0 is
+ * a no-op.  The plan array is read before the call returns; the buffers must
+ * stay alive until the stream has passed the copies.
+ */
+nsd_status nsd_copy_plan(const void* src, int64_t src_bytes, void* dst, int64_t dst_bytes,
+                         const int64_t* copies, int64_t n_copies, int64_t chunk_bytes,
+                         int32_t direction, void* stream);
 
 /*
  * Speculative acceptance with residual resampling.

@@ -41,6 +41,7 @@ _SIGS = {
                                            _I32, _I32, _I32, _I32, _I32, _I32, _I32, _F32, _P,
                                            _P, _SZ, _P]),
     "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
+    "nsd_copy_plan": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I32, _P]),
 }
 
 
@@ -238,6 +239,32 @@ def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, acce
     return accepted_len, out_tokens
 
 
+COPY_H2D, COPY_D2H = 1, 2
+DEFAULT_CHUNK = 32 << 20   # bytes per DMA submission
+
+
+def copy_plan(src, dst, copies, chunk_bytes=DEFAULT_CHUNK, stream=None):
+    """Execute a KV copy plan between a pinned host tensor and a device tensor.
+
+    copies: int64 array [n][3] of (source byte offset, destination byte offset,
+    bytes).  The direction follows the tensors' devices; the host tensor must be
+    pinned.  Runs on ``stream`` (a torch.cuda.Stream) or the current stream."""
+    import numpy as np
+    if src.is_cuda == dst.is_cuda:
+        raise ValueError("copy_plan moves between a pinned host tensor and a device tensor")
+    host, dev = (src, dst) if dst.is_cuda else (dst, src)
+    if not host.is_pinned():
+        raise ValueError("the host tensor must be pinned (pin_memory=True)")
+    if not (src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("src and dst must be contiguous")
+    plan = np.ascontiguousarray(np.asarray(copies, dtype=np.int64).reshape(-1, 3))
+    st = (stream or torch.cuda.current_stream(dev.device)).cuda_stream
+    _check("copy_plan", lib().nsd_copy_plan(
+        _ptr(src), src.numel() * src.element_size(), _ptr(dst), dst.numel() * dst.element_size(),
+        plan.ctypes.data if len(plan) else None, len(plan), int(chunk_bytes),
+        COPY_H2D if dst.is_cuda else COPY_D2H, st))
+
+
 __all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
-           "new_workspace", "gather_verify_attention",
-           "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]
+           "new_workspace", "gather_verify_attention", "copy_plan", "COPY_H2D", "COPY_D2H",
+           "DEFAULT_CHUNK", "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

@@ -90,3 +90,18 @@ def test_accept_validation(lib):
     assert f(None, None, None, None, None, 4, 1000, 64, None, None, None) == 3
     assert f(None, None, None, None, None, 0, 1000, 4, None, None, None) == 0
     assert f(None, None, None, None, None, 4, 1000, 4, None, None, None) == 1
+
+
+def test_copy_plan_validation(lib):
+    f = lib.nsd_copy_plan
+    plan = (ctypes.c_int64 * 6)(0, 0, 64, 64, 64, 64)
+    fake = ctypes.c_void_p(16)  # never dereferenced: every case fails before any copy
+    assert f(fake, 128, fake, 128, plan, 2, 1 << 20, 3, None) == 2          # bad direction
+    assert f(fake, 128, fake, 128, plan, 2, 0, 1, None) == 2                # chunk < 1
+    assert f(fake, 128, fake, 128, plan, -1, 1 << 20, 1, None) == 2         # n < 0
+    assert f(None, 128, None, 128, None, 0, 1 << 20, 1, None) == 0          # empty plan
+    assert f(None, 128, fake, 128, plan, 2, 1 << 20, 1, None) == 1          # NULL
+    assert f(fake, 100, fake, 128, plan, 2, 1 << 20, 1, None) == 2          # src overrun
+    assert b"leaves its buffers" in lib.nsd_last_error()
+    bad = (ctypes.c_int64 * 3)(0, -8, 8)
+    assert f(fake, 128, fake, 128, bad, 1, 1 << 20, 2, None) == 2          # negative offset

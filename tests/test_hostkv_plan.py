@@ -1,0 +1,65 @@
+"""Host-side logic of the HostKV preparation (no GPU): the arena layout keeps
+each request's logical KV at its extent, and the H2D plan maps every arriving
+block from its arena block to the staging id its stage table names, matching
+the gather's (staging id, pool id) pairs."""
+import numpy as np
+import torch
+
+from paper_2609_29364_amd.hostkv import h2d_plan
+from workload import CONFIGS, custom_config, make_meta, make_layer, make_hostkv
+from workload.synth import logical_kv
+from workload.layout import logical_kv_from_blocks
+
+
+def _round(cfg):
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    return meta, lay, make_hostkv(cfg, meta, lay, pin=False)
+
+
+def test_arena_holds_every_request_at_its_extent():
+    for cfg in (CONFIGS["tiny"], custom_config(staging_order="shuffled", seed=10)):
+        meta, lay, host = _round(cfg)
+        # extents are disjoint and within the arena
+        order = np.argsort(host.extent)
+        ends = host.extent[order] + host.capacity[order]
+        assert np.all(host.extent[order][1:] >= ends[:-1]) and ends[-1] <= host.k.shape[0]
+        for r in range(meta.bs):
+            n = meta.nblk(r)
+            assert host.capacity[r] >= n
+            kb, vb = host.k[host.extent[r]:host.extent[r] + n], host.v[host.extent[r]:host.extent[r] + n]
+            k, v = logical_kv_from_blocks(kb, vb, int(meta.seq_lens[r]))
+            k0, v0 = logical_kv(meta, lay, r)
+            assert torch.equal(k.view(torch.int16), k0.view(torch.int16))
+            assert torch.equal(v.view(torch.int16), v0.view(torch.int16))
+
+
+def test_plan_moves_each_arriving_block_to_its_staging_id():
+    cfg = custom_config(staging_order="shuffled", seed=11, bs=6, n_arriving=4, pool_blocks=None)
+    meta, lay, host = _round(cfg)
+    bb = host.k[0].numel() * 2
+    plan = h2d_plan(host.extent, meta.stage_table, meta.arriving, meta.seq_lens, bb)
+    # brute force: one triple per arriving block, in request order
+    want = []
+    for r in range(meta.bs):
+        if not meta.arriving[r]:
+            continue
+        for j in range(meta.nblk(r)):
+            want.append(((host.extent[r] + j) * bb, meta.stage_table[r, j] * bb, bb))
+    assert np.array_equal(plan, np.array(want, dtype=np.int64))
+    # the destination blocks are exactly the gather's staging ids, each once
+    assert sorted((plan[:, 1] // bb).tolist()) == sorted(meta.src_ids.tolist())
+    # applying the plan on the host reproduces the staging pool at those ids
+    hk = host.k.view(torch.uint8).numpy().reshape(-1)
+    st = np.zeros(lay.k_stage.numel() * 2, dtype=np.uint8)
+    for s, d, n in plan:
+        st[d:d + n] = hk[s:s + n]
+    ref = lay.k_stage.view(torch.uint8).numpy().reshape(-1)
+    for i in meta.src_ids:
+        assert np.array_equal(st[i * bb:(i + 1) * bb], ref[i * bb:(i + 1) * bb])
+
+
+def test_plan_of_a_round_with_no_arrivals_is_empty():
+    cfg = custom_config(n_arriving=0, seed=12)
+    meta, lay, host = _round(cfg)
+    assert h2d_plan(host.extent, meta.stage_table, meta.arriving, meta.seq_lens, 4096).shape == (0, 3)

@@ -256,3 +256,48 @@ def make_accept(cfg: RoundConfig, meta: RoundMeta, device) -> Optional[AcceptDat
     u = torch.randint(0, 1 << 24, (nq,), generator=ug, device=device, dtype=torch.int64)
     u = u.to(torch.float32) * (2.0 ** -24)
     return AcceptData(p, qd, tok, u)
+
+
+@dataclass
+class HostKV:
+    """A pinned host KV arena for one layer (every request at a stable extent).
+
+    Request r owns blocks [extent[r], extent[r] + capacity[r]) of each plane;
+    its first ceil(L_r/16) blocks hold its logical KV (the staged blocks if it is
+    arriving, its pool blocks if resident), the rest is reserved headroom."""
+    k: torch.Tensor            # bf16 [arena_blocks][Hkv][D/8][16][8], pinned
+    v: torch.Tensor            # bf16 [arena_blocks][Hkv][D][16], pinned
+    extent: np.ndarray         # int64 [bs], first arena block of request r
+    capacity: np.ndarray       # int64 [bs], blocks reserved for request r
+
+
+def make_hostkv(cfg: RoundConfig, meta: RoundMeta, layer: LayerData, headroom_tokens: int = 64,
+                seed_stream: int = 97, pin: bool = True) -> HostKV:
+    """Host arena holding the round's KV the way HostKV keeps it: extents sized
+    for the tokens so far plus generation headroom (Eq. E.1), laid out in a seeded
+    order; the bytes come from the layer's staging pool and worker pool.  pin=False
+    (no GPU present) gives the same arena in pageable memory."""
+    nblk = -(-meta.seq_lens.astype(np.int64) // BLOCK_SIZE)
+    cap = -(-(meta.seq_lens.astype(np.int64) + headroom_tokens) // BLOCK_SIZE)
+    order = _np_rng(cfg.seed, seed_stream).permutation(meta.bs)
+    extent = np.zeros(meta.bs, dtype=np.int64)
+    off = 0
+    for r in order:
+        extent[r] = off
+        off += int(cap[r])
+    kshape, vshape = tuple(layer.k_pool.shape[1:]), tuple(layer.v_pool.shape[1:])
+    hk = torch.zeros((off,) + kshape, dtype=torch.bfloat16, pin_memory=pin)
+    hv = torch.zeros((off,) + vshape, dtype=torch.bfloat16, pin_memory=pin)
+    src_k, src_v = layer.k_pool.cpu(), layer.v_pool.cpu()
+    stg_k, stg_v = layer.k_stage.cpu(), layer.v_stage.cpu()
+    for r in range(meta.bs):
+        n = int(nblk[r])
+        if meta.arriving[r]:
+            ids = torch.as_tensor(meta.stage_table[r, :n], dtype=torch.long)
+            hk[extent[r]:extent[r] + n] = stg_k[ids]
+            hv[extent[r]:extent[r] + n] = stg_v[ids]
+        else:
+            ids = torch.as_tensor(meta.block_table[r, :n], dtype=torch.long)
+            hk[extent[r]:extent[r] + n] = src_k[ids]
+            hv[extent[r]:extent[r] + n] = src_v[ids]
+    return HostKV(hk, hv, extent, cap)
