@@ -35,6 +35,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy three times (counter calibration)")
+    ap.add_argument("--h2d", action="store_true",
+                    help="measure the preparation from a pinned host arena instead: H2D rate, "
+                         "interference with the round (Eq. D.1) and exposed KV-ready wait of "
+                         "double-banked rounds (Eq. G.1)")
     return ap.parse_args()
 
 
@@ -153,6 +157,131 @@ def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
                       f"{t_total:.1f} s of fp64 numpy"}
 
 
+def h2d_bench(args):
+    """Preparation from HostKV: one JSON line (not the headline metric).
+
+    * h2d: the round's arriving KV copied from the pinned arena into a bank alone.
+    * interference (Eq. D.1): mean round time (fused pass + acceptance) while the next
+      round's H2D runs on the copy stream, against the same rounds with no copy.
+    * pipeline (Eq. G.1): double-banked rounds, each needing its own H2D of the first n
+      arriving requests' blocks; inputs ready at t = 0, the worker ready when the
+      previous round ends, KV ready when its H2D ends; exposed wait = [KV ready -
+      max(input ready, worker ready)]+ per round, and rounds/s."""
+    import torch
+    import paper_2609_29364_amd as nsd
+    from paper_2609_29364_amd.hostkv import DoubleBank, h2d_plan
+    from workload import CONFIGS, make_meta, make_layer, make_accept, make_hostkv
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.workload]
+    meta = make_meta(cfg)
+    layer = make_layer(cfg, meta, 0, dev)
+    acc_in = make_accept(cfg, meta, dev)
+    host = make_hostkv(cfg, meta, layer)
+    i32 = lambda a: torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32, device=dev)
+    bt, st, sl, qi = (i32(meta.block_table), i32(meta.stage_table), i32(meta.seq_lens),
+                      i32(meta.q_indptr))
+    bb = layer.k_stage[0].numel() * 2
+    plan_all = h2d_plan(host.extent, meta.stage_table, meta.arriving, meta.seq_lens, bb)
+    bank = DoubleBank(layer.k_stage.shape, layer.v_stage.shape, dev)
+    del layer.k_stage, layer.v_stage
+    out = torch.empty_like(layer.q)
+    ws = nsd.new_workspace(nsd.verify_attention_workspace_size(
+        cfg.bs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, meta.max_q, meta.max_seq_len), dev)
+    acc_len = torch.empty(cfg.bs, dtype=torch.int32, device=dev)
+    toks = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
+    comp = torch.cuda.current_stream(dev)
+
+    def round_(i):
+        ks, vs = bank.bank(i)
+        nsd.gather_verify_attention(layer.q, layer.k_pool, layer.v_pool, ks, vs, bt, st, sl, qi,
+                                    meta.max_q, meta.max_seq_len, out=out, workspace=ws)
+        if acc_in is not None:
+            nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
+                            acc_in.uniforms, qi, cfg.k_hi, accepted_len=acc_len, out_tokens=toks)
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    # H2D alone (both banks filled, so every round below reads valid staging)
+    for i in range(2):
+        bank.prepare(i, host.k, host.v, plan_all, plan_all)
+    torch.cuda.synchronize()
+    h2d_bytes = 2 * int(plan_all[:, 2].sum())
+    t = []
+    for _ in range(3):
+        s0 = ev(); s0.record(bank.copy_stream)
+        e1 = bank.prepare(0, host.k, host.v, plan_all, plan_all)
+        torch.cuda.synchronize()
+        t.append(s0.elapsed_time(e1))
+    h2d_ms = float(np.median(t))
+
+    # interference (Eq. D.1): rounds on bank 0 with and without bank 1 being filled
+    def timed_rounds(n):
+        e = [ev() for _ in range(n + 1)]
+        e[0].record(comp)
+        for k in range(n):
+            round_(0)
+            e[k + 1].record(comp)
+        return e
+    for _ in range(args.warmup):
+        round_(0)
+    torch.cuda.synchronize()
+    eb = timed_rounds(args.steps)
+    torch.cuda.synchronize()
+    t_base = eb[0].elapsed_time(eb[-1]) / args.steps
+    n_ov = max(4, int(h2d_ms / t_base * 0.8))     # rounds that fit inside one H2D
+    s0 = ev(); s0.record(bank.copy_stream)
+    e_h2d = bank.prepare(1, host.k, host.v, plan_all, plan_all)
+    eo = timed_rounds(n_ov)
+    torch.cuda.synchronize()
+    # count only the rounds that ended before the copy did
+    ends = [s0.elapsed_time(x) for x in eo]
+    h_end = s0.elapsed_time(e_h2d)
+    inside = [k for k in range(n_ov) if ends[k + 1] <= h_end]
+    t_overlap = (float(np.mean([ends[k + 1] - ends[k] for k in inside])) if inside else None)
+
+    # pipeline (Eq. G.1) for a few arrival volumes per round
+    order = [r for r in range(meta.bs) if meta.arriving[r]]
+    pipeline = []
+    for n_arr in sorted({1, 4, 16, len(order)}):
+        keep = np.zeros(meta.bs, dtype=bool)
+        keep[order[:n_arr]] = True
+        plan = h2d_plan(host.extent, meta.stage_table, keep, meta.seq_lens, bb)
+        rounds = 12
+        torch.cuda.synchronize()
+        t0 = ev(); t0.record(comp)
+        bank.copy_stream.wait_event(t0)
+        h_ev, r_ev = [], []
+        bank.prepare(0, host.k, host.v, plan, plan)
+        h_ev.append(bank.ready(0))
+        for i in range(rounds):
+            if i + 1 < rounds:
+                bank.prepare(i + 1, host.k, host.v, plan, plan)
+                h_ev.append(bank.ready(i + 1))
+            comp.wait_event(bank.ready(i))
+            round_(i)
+            bank.done(i, comp)
+            e = ev(); e.record(comp); r_ev.append(e)
+        torch.cuda.synchronize()
+        H = [t0.elapsed_time(x) for x in h_ev]
+        R = [t0.elapsed_time(x) for x in r_ev]
+        W = [0.0] + R[:-1]
+        E = [max(0.0, H[i] - W[i]) for i in range(rounds)]
+        pipeline.append({"arriving_per_round": n_arr, "h2d_mb": round(2 * int(plan[:, 2].sum()) / 2**20, 2),
+                         "exposed_wait_ms_mean": round(float(np.mean(E[1:])), 4),
+                         "rounds_per_s": round((rounds - 1) / ((R[-1] - R[0]) * 1e-3), 1)})
+    res = {"mode": "h2d", "workload": cfg.name, "arriving": int(meta.arriving.sum()),
+           "h2d": {"bytes": h2d_bytes, "ms": round(h2d_ms, 3),
+                   "gbs": round(h2d_bytes / (h2d_ms * 1e-3) / 1e9, 2),
+                   "chunk_bytes": nsd.DEFAULT_CHUNK, "copies_in_plan": int(len(plan_all))},
+           "interference": {"t_base_ms": round(t_base, 4),
+                            "t_overlap_ms": None if t_overlap is None else round(t_overlap, 4),
+                            "rounds_inside_copy": len(inside),
+                            "delta_t": None if t_overlap is None else round((t_overlap - t_base) / t_base, 4)},
+           "pipeline": pipeline}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -160,6 +289,9 @@ def main():
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.h2d:
+        h2d_bench(args)
         return
     import torch
     import paper_2609_29364_amd as nsd
