@@ -10,6 +10,9 @@ Plain, slow, fp64 numpy restatements of what the round computes:
                    of the speculative-decoding works the paper builds on
                    (Leviathan et al. 2023; Chen et al. 2023; cited in
                    Sections 1 and 2; the paper does not restate it).
+* ``commit``    -- closing the round: appending the window's K/V to the paged
+                   cache, committed lengths, and the suffix written back to the
+                   host arena (Section 3; Section 5; Appendix E.1).
 
 Only the test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library
@@ -20,6 +23,6 @@ Every function is pinned by ``tests/test_oracle_*.py`` against a library
 routine, closed forms, invariants or a sampling theorem; none is "parity
 unpinned".
 """
-from . import gather, attention, accept
+from . import gather, attention, accept, commit
 
-__all__ = ["gather", "attention", "accept"]
+__all__ = ["gather", "attention", "accept", "commit"]
