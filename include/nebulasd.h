@@ -223,6 +223,55 @@ nsd_status nsd_copy_plan(const void* src, int64_t src_bytes, void* dst, int64_t 
                          int32_t direction, void* stream);
 
 /*
+ * Append the window's new K/V rows to the paged cache, for one layer.
+ *
+ * Passage: Section 3 (the cache is paged and append-dominant: an iteration
+ * only adds the K/V of the tokens it processed).
+ *
+ * Row q_indptr[r] + j of k_new / v_new (bf16 [total_q][num_kv_heads][head_dim])
+ * is window token j of request r, at position t = seq_lens[r] - n_q + j; it is
+ * written to slot t % 16 of block block_table[r][t / 16] of k_pool / v_pool
+ * (this layer's planes, layout above), every KV head.  Nothing else is
+ * written.  Positions outside [0, 16 * max_blocks_per_seq) and block ids
+ * outside [0, num_blocks) are skipped.  block_size == 16, head_dim in {64, 128}.
+ * bs == 0 or total_q == 0 is a no-op.
+ */
+nsd_status nsd_kv_append(void* k_pool, void* v_pool, int64_t num_blocks, const void* k_new,
+                         const void* v_new, const int32_t* block_table,
+                         int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                         const int32_t* q_indptr, int32_t bs, int32_t total_q,
+                         int32_t num_kv_heads, int32_t block_size, int32_t head_dim,
+                         void* stream);
+
+/*
+ * Commit accepted lengths: new_lens[r] = seq_lens[r] - K_r + n_r, with
+ * K_r = q_indptr[r+1] - q_indptr[r] - 1 and n_r = accepted_len[r] clamped to
+ * [0, K_r].  The request keeps its anchor and its accepted proposals; the
+ * resampled or bonus token is the next round's anchor.
+ *
+ * Passage: Sections 1 and 3 (verified tokens are committed; the cache only
+ * grows by what an iteration adds); Section 5 (HostKV records each
+ * request's valid sequence length).
+ * All pointers device, int32 [bs] (q_indptr [bs+1]); new_lens may alias
+ * seq_lens.  bs == 0 is a no-op.
+ */
+nsd_status nsd_commit_lengths(const int32_t* seq_lens, const int32_t* q_indptr,
+                              const int32_t* accepted_len, int32_t* new_lens, int32_t bs,
+                              void* stream);
+
+/*
+ * Device address of pinned host memory (hipHostMalloc), so that kernels, such
+ * as nsd_kv_gather writing a request's KV suffix back into its HostKV extent,
+ * can read or write it directly.
+ *
+ * Passage: Section 5 and Appendix E.1 (incremental writeback of the valid
+ * suffix into the persistent pinned host arena).
+ * Returns NSD_ERR_UNSUPPORTED if `host` is not pinned memory mapped for the
+ * current device.
+ */
+nsd_status nsd_host_alias(const void* host, void** device_alias);
+
+/*
  * Speculative acceptance with residual resampling.
  *
  * Passage: Sections 1 and 2 (speculative decoding as in Leviathan et al. 2023

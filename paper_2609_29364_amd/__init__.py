@@ -42,6 +42,10 @@ _SIGS = {
                                            _P, _SZ, _P]),
     "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
     "nsd_copy_plan": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I32, _P]),
+    "nsd_kv_append": (_I32, [_P, _P, _I64, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _I32, _I32,
+                             _P]),
+    "nsd_commit_lengths": (_I32, [_P, _P, _P, _P, _I32, _P]),
+    "nsd_host_alias": (_I32, [_P, ctypes.POINTER(ctypes.c_void_p)]),
 }
 
 
@@ -265,6 +269,59 @@ def copy_plan(src, dst, copies, chunk_bytes=DEFAULT_CHUNK, stream=None):
         COPY_H2D if dst.is_cuda else COPY_D2H, st))
 
 
+def kv_append(k_pool, v_pool, k_new, v_new, block_table, seq_lens, q_indptr):
+    """Write the window rows k_new/v_new [total_q][Hkv][D] into their paged slots (one layer)."""
+    for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool"), (k_new, "k_new"), (v_new, "v_new")):
+        _dev(t, torch.bfloat16, n)
+    for t, n in ((block_table, "block_table"), (seq_lens, "seq_lens"), (q_indptr, "q_indptr")):
+        _dev(t, torch.int32, n)
+    total_q, hkv, d = k_new.shape
+    if v_new.shape != k_new.shape or k_pool.shape[1] != hkv:
+        raise ValueError("k_new/v_new must be [total_q][Hkv][D] matching the pools")
+    _check("kv_append", lib().nsd_kv_append(
+        _ptr(k_pool), _ptr(v_pool), k_pool.shape[0], _ptr(k_new), _ptr(v_new), _ptr(block_table),
+        block_table.shape[1], _ptr(seq_lens), _ptr(q_indptr), seq_lens.numel(), total_q, hkv,
+        BLOCK_SIZE, d, _stream(k_pool)))
+
+
+def commit_lengths(seq_lens, q_indptr, accepted_len, out=None):
+    """Committed lengths seq_lens - K + accepted_len (int32 [bs])."""
+    for t, n in ((seq_lens, "seq_lens"), (q_indptr, "q_indptr"), (accepted_len, "accepted_len")):
+        _dev(t, torch.int32, n)
+    if out is None:
+        out = torch.empty_like(seq_lens)
+    _check("commit_lengths", lib().nsd_commit_lengths(
+        _ptr(seq_lens), _ptr(q_indptr), _ptr(accepted_len), _ptr(out), seq_lens.numel(),
+        _stream(seq_lens)))
+    return out
+
+
+def host_alias(t):
+    """Device address of a pinned host tensor's data."""
+    if t.is_cuda or not t.is_pinned():
+        raise ValueError("host_alias needs a pinned host tensor")
+    p = ctypes.c_void_p()
+    _check("host_alias", lib().nsd_host_alias(_ptr(t), ctypes.byref(p)))
+    return p.value
+
+
+def kv_writeback(k_pool, v_pool, host_k, host_v, src_ids, dst_ids):
+    """Copy whole pool blocks src_ids[i] into blocks dst_ids[i] of a pinned host arena
+    (same block layout), by the gather kernel writing through the arena's device alias."""
+    _dev(k_pool, torch.bfloat16, "k_pool")
+    _dev(v_pool, torch.bfloat16, "v_pool")
+    _dev(src_ids, torch.int32, "src_ids")
+    _dev(dst_ids, torch.int32, "dst_ids")
+    if host_k.shape[1:] != k_pool.shape[1:] or host_v.shape[1:] != v_pool.shape[1:]:
+        raise ValueError("the arena must have the pool's block layout")
+    hkv, d = k_pool.shape[1], v_pool.shape[2]
+    _check("kv_writeback", lib().nsd_kv_gather(
+        _ptr(k_pool), _ptr(v_pool), k_pool.shape[0], host_alias(host_k), host_alias(host_v),
+        host_k.shape[0], _ptr(src_ids), _ptr(dst_ids), src_ids.numel(), 1, 0, 1, hkv,
+        BLOCK_SIZE, d, _stream(k_pool)))
+
+
 __all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
            "new_workspace", "gather_verify_attention", "copy_plan", "COPY_H2D", "COPY_D2H",
-           "DEFAULT_CHUNK", "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]
+           "DEFAULT_CHUNK", "kv_append", "commit_lengths", "host_alias", "kv_writeback",
+           "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

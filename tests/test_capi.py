@@ -105,3 +105,19 @@ def test_copy_plan_validation(lib):
     assert b"leaves its buffers" in lib.nsd_last_error()
     bad = (ctypes.c_int64 * 3)(0, -8, 8)
     assert f(fake, 128, fake, 128, bad, 1, 1 << 20, 2, None) == 2          # negative offset
+
+
+def test_append_commit_alias_validation(lib):
+    f = lib.nsd_kv_append
+    fake = ctypes.c_void_p(16)
+    assert f(fake, fake, 8, fake, fake, fake, 4, fake, fake, 2, 8, 2, 8, 64, None) == 3    # block size
+    assert f(fake, fake, 8, fake, fake, fake, 4, fake, fake, 2, 8, 2, 16, 96, None) == 3   # head_dim
+    assert f(fake, fake, 8, fake, fake, fake, 0, fake, fake, 2, 8, 2, 16, 64, None) == 2   # no blocks
+    assert f(None, None, 8, None, None, None, 4, None, None, 0, 8, 2, 16, 64, None) == 0   # bs == 0
+    assert f(None, fake, 8, fake, fake, fake, 4, fake, fake, 2, 8, 2, 16, 64, None) == 1   # NULL
+    g = lib.nsd_commit_lengths
+    assert g(None, None, None, None, 0, None) == 0
+    assert g(None, None, None, None, -1, None) == 2
+    assert g(fake, None, fake, fake, 3, None) == 1
+    out = ctypes.c_void_p()
+    assert lib.nsd_host_alias(None, ctypes.byref(out)) == 1

@@ -1,0 +1,91 @@
+"""Closing the round on the GPU: the window append, the committed lengths and
+the suffix writeback into the pinned host arena, each against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_29364_amd as nsd
+from workload import CONFIGS, custom_config, make_meta, make_layer, make_accept, make_hostkv
+from parity import i32, u16
+
+pytestmark = pytest.mark.gpu
+
+
+def _rows(meta, cfg, seed):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    shape = (meta.total_q, cfg.num_kv_heads, cfg.head_dim)
+    return (torch.randn(shape, generator=g).to(torch.bfloat16),
+            torch.randn(shape, generator=g).to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("cfg", [CONFIGS["tiny"],
+                                 custom_config(seed=41, bs=7, k_lo=1, k_hi=6, head_dim=128,
+                                               num_q_heads=8, num_kv_heads=4, pool_blocks=None)],
+                         ids=["tiny", "ragged_d128"])
+def test_append_matches_oracle(device, cfg):
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    kn, vn = _rows(meta, cfg, 3)
+    kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
+    nsd.kv_append(kp, vp, kn.to(device), vn.to(device), i32(meta.block_table, device),
+                  i32(meta.seq_lens, device), i32(meta.q_indptr, device))
+    torch.cuda.synchronize()
+    rk, rv = oracle.commit.kv_append(u16(lay.k_pool), u16(lay.v_pool), u16(kn), u16(vn),
+                                     meta.block_table, meta.seq_lens, meta.q_indptr)
+    assert np.array_equal(u16(kp), rk) and np.array_equal(u16(vp), rv)
+
+
+def test_commit_lengths_matches_oracle(device):
+    cfg = custom_config(seed=42, bs=50, k_lo=0, k_hi=8, pool_blocks=None, ctx_lo=20, ctx_hi=90)
+    meta = make_meta(cfg)
+    g = np.random.default_rng(2)
+    acc = g.integers(-2, 11, meta.bs).astype(np.int32)      # out-of-range values are clamped
+    out = nsd.commit_lengths(i32(meta.seq_lens, device), i32(meta.q_indptr, device),
+                             i32(acc, device))
+    torch.cuda.synchronize()
+    k = np.diff(meta.q_indptr) - 1
+    ref = oracle.commit.commit_lengths(meta.seq_lens, meta.q_indptr, np.clip(acc, 0, k))
+    assert np.array_equal(out.cpu().numpy(), ref)
+
+
+def test_round_close_writes_back_the_suffix(device):
+    # round -> acceptance -> commit -> suffix writeback into the host arena
+    cfg = custom_config(seed=43, bs=6, k_lo=2, k_hi=5, n_arriving=2, pool_blocks=None)
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    host = make_hostkv(cfg, meta, lay)
+    arena0 = (u16(host.k).copy(), u16(host.v).copy())
+    kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
+    nsd.kv_gather(lay.k_stage.to(device), lay.v_stage.to(device), kp, vp,
+                  i32(meta.src_ids, device), i32(meta.dst_ids, device))
+    acc_in = make_accept(cfg, meta, device)
+    acc, _ = nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
+                             acc_in.uniforms, i32(meta.q_indptr, device), int(meta.depth.max()))
+    new_len = nsd.commit_lengths(i32(meta.seq_lens, device), i32(meta.q_indptr, device), acc)
+    torch.cuda.synchronize()
+    new_len = new_len.cpu().numpy()
+    host_len = meta.seq_lens - (np.diff(meta.q_indptr))      # the window is new this round
+    src, dst = oracle.commit.writeback_pairs(meta.block_table, host.extent, host_len, new_len)
+    nsd.kv_writeback(kp, vp, host.k, host.v, i32(src, device), i32(dst, device))
+    torch.cuda.synchronize()
+    pool_k, pool_v = u16(kp.cpu()), u16(vp.cpu())
+    ref_k, ref_v = arena0[0].copy(), arena0[1].copy()
+    ref_k[dst], ref_v[dst] = pool_k[src], pool_v[src]
+    assert np.array_equal(u16(host.k), ref_k) and np.array_equal(u16(host.v), ref_v)
+    # the arena now holds every request's committed tokens
+    from workload.layout import logical_kv_from_blocks
+    from workload.synth import logical_kv
+    for r in range(meta.bs):
+        n = -(-int(new_len[r]) // 16)
+        e = int(host.extent[r])
+        k, v = logical_kv_from_blocks(host.k[e:e + n], host.v[e:e + n], int(new_len[r]))
+        k0, v0 = logical_kv(meta, lay, r)
+        assert torch.equal(k.view(torch.int16), k0[:int(new_len[r])].view(torch.int16))
+
+
+def test_host_alias_refuses_pageable(device):
+    with pytest.raises(ValueError):
+        nsd.host_alias(torch.zeros(16))
+    t = torch.zeros(64, pin_memory=True)
+    assert nsd.host_alias(t) is not None
