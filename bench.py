@@ -270,6 +270,34 @@ def h2d_bench(args):
         pipeline.append({"arriving_per_round": n_arr, "h2d_mb": round(2 * int(plan[:, 2].sum()) / 2**20, 2),
                          "exposed_wait_ms_mean": round(float(np.mean(E[1:])), 4),
                          "rounds_per_s": round((rounds - 1) / ((R[-1] - R[0]) * 1e-3), 1)})
+    # closing the round: window append, committed lengths, suffix writeback to the arena
+    kn = torch.randn((meta.total_q, cfg.num_kv_heads, cfg.head_dim), device=dev).to(torch.bfloat16)
+    vn = torch.randn_like(kn)
+    round_(0)
+    new_len = nsd.commit_lengths(sl, qi, acc_len) if acc_in is not None else sl.clone()
+    torch.cuda.synchronize()
+    nl = new_len.cpu().numpy()
+    host_len = meta.seq_lens - np.diff(meta.q_indptr)        # the window is new this round
+    from paper_2609_29364_amd.hostkv import writeback_pairs
+    wsrc, wdst = writeback_pairs(meta.block_table, host.extent, host_len, nl)
+    wsrc_d, wdst_d = i32(wsrc), i32(wdst)
+    close = {}
+    for name, fn in (("append", lambda: nsd.kv_append(layer.k_pool, layer.v_pool, kn, vn, bt, sl, qi)),
+                     ("commit", lambda: nsd.commit_lengths(sl, qi, acc_len, out=new_len)),
+                     ("writeback", lambda: nsd.kv_writeback(layer.k_pool, layer.v_pool, host.k,
+                                                            host.v, wsrc_d, wdst_d))):
+        fn(); torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(comp)
+        for _ in range(10):
+            fn()
+        b.record(comp)
+        torch.cuda.synchronize()
+        close[name + "_ms"] = round(a.elapsed_time(b) / 10, 4)
+    wb_bytes = 2 * len(wsrc) * bb
+    close["writeback_bytes"] = wb_bytes
+    close["writeback_gbs"] = round(wb_bytes / (close["writeback_ms"] * 1e-3) / 1e9, 2)
+    close["append_bytes"] = 2 * kn.numel() * 2
     res = {"mode": "h2d", "workload": cfg.name, "arriving": int(meta.arriving.sum()),
            "h2d": {"bytes": h2d_bytes, "ms": round(h2d_ms, 3),
                    "gbs": round(h2d_bytes / (h2d_ms * 1e-3) / 1e9, 2),
@@ -278,7 +306,7 @@ def h2d_bench(args):
                             "t_overlap_ms": None if t_overlap is None else round(t_overlap, 4),
                             "rounds_inside_copy": len(inside),
                             "delta_t": None if t_overlap is None else round((t_overlap - t_base) / t_base, 4)},
-           "pipeline": pipeline}
+           "pipeline": pipeline, "close": close}
     print(json.dumps(res), flush=True)
 
 

@@ -75,3 +75,19 @@ class DoubleBank:
 
     def bank(self, i):
         return self.k[i % 2], self.v[i % 2]
+
+
+def writeback_pairs(block_table, extent, host_len, new_len):
+    """(pool block id, arena block id) int32 pairs of the suffix each request writes
+    back: the blocks holding its tokens host_len .. new_len - 1 (Section 5:
+    incremental writeback of the valid suffix; Appendix E.1 extents)."""
+    host_len = np.asarray(host_len, dtype=np.int64)
+    new_len = np.asarray(new_len, dtype=np.int64)
+    src, dst = [], []
+    for r in np.nonzero(new_len > host_len)[0]:
+        j = np.arange(host_len[r] // BLOCK, (new_len[r] - 1) // BLOCK + 1)
+        src.append(np.asarray(block_table[r, j], dtype=np.int64))
+        dst.append(int(extent[r]) + j)
+    if not src:
+        return np.zeros(0, np.int32), np.zeros(0, np.int32)
+    return np.concatenate(src).astype(np.int32), np.concatenate(dst).astype(np.int32)

@@ -63,3 +63,19 @@ def test_plan_of_a_round_with_no_arrivals_is_empty():
     cfg = custom_config(n_arriving=0, seed=12)
     meta, lay, host = _round(cfg)
     assert h2d_plan(host.extent, meta.stage_table, meta.arriving, meta.seq_lens, 4096).shape == (0, 3)
+
+
+def test_writeback_pairs_match_the_oracle():
+    import oracle
+    from paper_2609_29364_amd.hostkv import writeback_pairs
+    g = np.random.default_rng(4)
+    bs = 30
+    bt = g.permutation(bs * 16).reshape(bs, 16).astype(np.int32)
+    extent = np.cumsum(np.r_[0, g.integers(17, 20, bs - 1)])
+    host = g.integers(0, 180, bs)
+    new = host + g.integers(0, 60, bs)
+    new = np.minimum(new, 256)
+    new[3] = host[3]
+    s1, d1 = writeback_pairs(bt, extent, host, new)
+    s2, d2 = oracle.commit.writeback_pairs(bt, extent, host, new)
+    assert np.array_equal(s1, s2) and np.array_equal(d1, d2)
