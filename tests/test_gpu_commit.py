@@ -89,3 +89,48 @@ def test_host_alias_refuses_pageable(device):
         nsd.host_alias(torch.zeros(16))
     t = torch.zeros(64, pin_memory=True)
     assert nsd.host_alias(t) is not None
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_round_with_window_append(device, fused):
+    # the pools start with the window slots poisoned; the round appends the window rows
+    # (the logical K/V at the window positions) before attention, which must then match
+    # the oracle on the logical cache; the committed lengths follow acceptance
+    from paper_2609_29364_amd.round import verify_round
+    from workload.synth import logical_kv
+    cfg = custom_config(seed=44, bs=5, k_lo=1, k_hi=5, n_arriving=2, pool_blocks=None)
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    kn = torch.empty((meta.total_q, cfg.num_kv_heads, cfg.head_dim), dtype=torch.bfloat16)
+    vn = torch.empty_like(kn)
+    kp, vp = lay.k_pool.clone(), lay.v_pool.clone()
+    ks, vs = lay.k_stage.clone(), lay.v_stage.clone()
+    for r in range(meta.bs):
+        a, b = int(meta.q_indptr[r]), int(meta.q_indptr[r + 1])
+        L = int(meta.seq_lens[r])
+        k, v = logical_kv(meta, lay, r)
+        kn[a:b], vn[a:b] = k[L - (b - a):], v[L - (b - a):]
+        # poison the window slots wherever this request's blocks live now
+        table = meta.stage_table if meta.arriving[r] else meta.block_table
+        pk, pv = (ks, vs) if meta.arriving[r] else (kp, vp)
+        for t in range(L - (b - a), L):
+            blk = int(table[r, t // 16])
+            pk[blk, :, :, t % 16, :] = float("nan")
+            pv[blk, :, :, t % 16] = float("nan")
+    acc_in = make_accept(cfg, meta, device)
+    committed = torch.empty(meta.bs, dtype=torch.int32, device=device)
+    st = i32(meta.stage_table, device) if fused else None
+    outs, acc, _ = verify_round(
+        kp.to(device)[None].contiguous(), vp.to(device)[None].contiguous(),
+        ks.to(device)[None].contiguous(), vs.to(device)[None].contiguous(),
+        i32(meta.src_ids, device), i32(meta.dst_ids, device), lay.q.to(device)[None].contiguous(),
+        i32(meta.block_table, device), i32(meta.seq_lens, device), i32(meta.q_indptr, device),
+        meta.max_q, meta.max_seq_len,
+        accept=(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens, acc_in.uniforms,
+                int(meta.depth.max())),
+        stage_table=st, window_kv=[(kn.to(device), vn.to(device))], committed=committed)
+    torch.cuda.synchronize()
+    from parity import check_attention
+    check_attention(meta, lay, outs[0], range(meta.bs))
+    ref = oracle.commit.commit_lengths(meta.seq_lens, meta.q_indptr, acc.cpu().numpy())
+    assert np.array_equal(committed.cpu().numpy(), ref)
