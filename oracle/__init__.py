@@ -13,6 +13,9 @@ Plain, slow, fp64 numpy restatements of what the round computes:
 * ``commit``    -- closing the round: appending the window's K/V to the paged
                    cache, committed lengths, and the suffix written back to the
                    host arena (Section 3; Section 5; Appendix E.1).
+* ``draft``     -- the draft stage before verification (Eq. 1): K single-query
+                   decode steps over the draft cache and inverse-CDF sampling
+                   of each proposal.
 
 Only the test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library
@@ -23,6 +26,6 @@ Every function is pinned by ``tests/test_oracle_*.py`` against a library
 routine, closed forms, invariants or a sampling theorem; none is "parity
 unpinned".
 """
-from . import gather, attention, accept, commit
+from . import gather, attention, accept, commit, draft
 
-__all__ = ["gather", "attention", "accept", "commit"]
+__all__ = ["gather", "attention", "accept", "commit", "draft"]
