@@ -8,6 +8,8 @@ resident in HBM before timing starts.  Prints ONE JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload verify_8b] [--unfused]
                     [--no-cpu-baseline]
+    python bench.py --draft [--draft-steps 4] [--draft-vocab 151936]   (draft stage)
+    python bench.py --h2d                                              (host-arena preparation)
 """
 import argparse
 import json
@@ -28,7 +30,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="verify_8b")
+    ap.add_argument("--workload", default=None,
+                    help="verify_8b (default), or draft_decode with --draft")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--unfused", action="store_true",
                     help="kv_gather and verify_attention as separate kernels")
@@ -39,7 +42,15 @@ def parse():
                     help="measure the preparation from a pinned host arena instead: H2D rate, "
                          "interference with the round (Eq. D.1) and exposed KV-ready wait of "
                          "double-banked rounds (Eq. G.1)")
-    return ap.parse_args()
+    ap.add_argument("--draft", action="store_true",
+                    help="time the draft stage instead (Eq. 1): --draft-steps single-query "
+                         "decode steps (append, attention, sampling) on draft_decode")
+    ap.add_argument("--draft-steps", type=int, default=4)
+    ap.add_argument("--draft-vocab", type=int, default=151936)
+    args = ap.parse_args()
+    if args.workload is None:
+        args.workload = "draft_decode" if args.draft else "verify_8b"
+    return args
 
 
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_29364_amd", "csrc", "verify_attention.hip")
@@ -310,6 +321,166 @@ def h2d_bench(args):
     print(json.dumps(res), flush=True)
 
 
+def draft_bench(args):
+    """The draft stage: one JSON line (not the headline metric).
+
+    A step is one whole stage on one batch: preparation of the arriving
+    requests (fused into step 0's attention pass, or --unfused as a gather
+    first), then per proposal the append of the processed token's K/V, one
+    query of attention per request over its cache, and the inverse-CDF draw of
+    the proposal."""
+    import torch
+    import paper_2609_29364_amd as nsd
+    from paper_2609_29364_amd.round import draft_stage
+    from workload import CONFIGS, make_draft
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.workload]
+    K, V = args.draft_steps, args.draft_vocab
+    dd = make_draft(cfg, K, V, dev)
+    meta, layer = dd.meta, dd.layer
+    i32 = lambda a: torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32, device=dev)
+    bt, qi = i32(meta.block_table), i32(np.arange(cfg.bs + 1))
+    st, src, dst = i32(meta.stage_table), i32(meta.src_ids), i32(meta.dst_ids)
+    pool_table = torch.where(st[:, :1] >= 0, torch.full_like(bt, -1), bt)
+    stage_rows = torch.where(st[:, :1] >= 0, st, torch.full_like(st, -1))
+    max_len = int(meta.seq_lens.max())
+    ws = nsd.new_workspace(nsd.verify_attention_workspace_size(
+        cfg.bs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 1, max_len), dev)
+    out = torch.empty_like(dd.q)
+    tok = torch.empty((cfg.bs, K), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    kp, vp, ks, vs = layer.k_pool, layer.v_pool, layer.k_stage, layer.v_stage
+
+    def stage(ev=None):
+        # the same calls as round.draft_stage, with events between the kernels
+        if ev: ev[0].record(stream)
+        if args.unfused:
+            nsd.kv_gather(ks, vs, kp, vp, src, dst)
+        for i in range(K):
+            if ev: ev[1 + 3 * i].record(stream)
+            if i == 0 and not args.unfused:
+                nsd.kv_append(kp, vp, dd.k_new[0], dd.v_new[0], pool_table, dd.lens[0], qi)
+                nsd.kv_append(ks, vs, dd.k_new[0], dd.v_new[0], stage_rows, dd.lens[0], qi)
+            else:
+                nsd.kv_append(kp, vp, dd.k_new[i], dd.v_new[i], bt, dd.lens[i], qi)
+            if ev: ev[2 + 3 * i].record(stream)
+            if i == 0 and not args.unfused:
+                nsd.gather_verify_attention(dd.q[0], kp, vp, ks, vs, bt, st, dd.lens[0], qi, 1,
+                                            max_len, out=out[0], workspace=ws)
+            else:
+                nsd.verify_attention(dd.q[i], kp, vp, bt, dd.lens[i], qi, 1, max_len, out=out[i],
+                                     workspace=ws)
+            if ev: ev[3 + 3 * i].record(stream)
+            nsd.sample(dd.probs[:, i], dd.uniforms[i], out=tok[:, i])
+        if ev: ev[1 + 3 * K].record(stream)
+
+    def library_stage():
+        draft_stage(kp, vp, dd.q, dd.k_new, dd.v_new, dd.probs, dd.uniforms, bt, dd.lens, qi,
+                    max_len, k_stage=ks, v_stage=vs, stage_table=None if args.unfused else st,
+                    src_ids=src, dst_ids=dst, tokens=tok, out=out, workspace=ws)
+
+    # the timed region: the library's draft stage, back to back
+    for _ in range(args.warmup):
+        library_stage()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        library_stage()
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms_stage = start.elapsed_time(end) / args.steps
+    # per-kernel breakdown from the same calls with events between them
+    n_ev = 2 + 3 * K
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+           for _ in range(max(3, args.steps // 2))]
+    for e in evs:
+        stage(e)
+    torch.cuda.synchronize()
+    t = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(n_ev - 1)] for e in evs]).mean(0)
+    gather_ms = float(t[0])
+    append_ms = t[1::3][:K]
+    attn_ms = t[2::3][:K]
+    sample_ms = t[3::3][:K]
+
+    hkv, d, hq = cfg.num_kv_heads, cfg.head_dim, cfg.num_q_heads
+    token_bytes = 2 * hkv * d * 2
+    block_bytes = hkv * 16 * d * 2
+    lens = dd.lens.cpu().numpy().astype(np.int64)
+    qo = 2 * cfg.bs * hq * d * 2
+    attn_bytes = [int(lens[i].sum()) * token_bytes + qo for i in range(K)]
+    # step 0 of the fused path: resident tokens read, the staged blocks it covers read and written
+    nb0 = -(-lens[0] // 16)
+    arr = meta.arriving
+    fused0 = (int(lens[0][~arr].sum()) * token_bytes + 2 * 2 * int(nb0[arr].sum()) * block_bytes
+              + qo)
+    sample_bytes = cfg.bs * V * 4 + cfg.bs * 8
+    steady = [attn_bytes[i] / (attn_ms[i] * 1e-3) / 1e9 for i in range(1, K)]
+    dom_ms = float(np.mean(attn_ms[1:])) if K > 1 else float(attn_ms[0])
+    dom_bytes = float(np.mean(attn_bytes[1:])) if K > 1 else attn_bytes[0]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    res = {
+        "metric": "draft-stage requests/s (draft decode shape, K single-query steps); "
+                  "achieved HBM TB/s",
+        "mode": "draft",
+        "value": round(cfg.bs / (ms_stage * 1e-3), 1), "unit": "requests/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_stage, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": describe(cfg) | {"draft_steps": K, "vocab": V},
+        "path": "unfused" if args.unfused else "fused",
+        "breakdown_ms": {"kv_gather": round(gather_ms, 5) if args.unfused else 0.0,
+                         "kv_append": [round(float(x), 5) for x in append_ms],
+                         "attention": [round(float(x), 5) for x in attn_ms],
+                         "sample": [round(float(x), 5) for x in sample_ms]},
+        "step0_fused_tbs": None if args.unfused else
+                           round(fused0 / (attn_ms[0] * 1e-3) / 1e12, 3),
+        "decode_attention_tbs": [round(x / 1e3, 3) for x in steady],
+        "sample_tbs": round(sample_bytes / (float(np.mean(sample_ms)) * 1e-3) / 1e12, 3),
+        "roofline": {"bound": "hbm", "kernel": "verify_attention (one query per request)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "alg_bytes_per_launch": int(dom_bytes)},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = draft_cpu_baseline(cfg, dd, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+def draft_cpu_baseline(cfg, dd, budget_s):
+    """The draft-stage oracle, untuned, on a bounded sample of the requests."""
+    import oracle
+    from workload.synth import logical_kv
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    order = np.random.default_rng(0).permutation(cfg.bs)
+    done, t_total = 0, 0.0
+    scale = 1.0 / np.sqrt(cfg.head_dim)
+    for r in order:
+        k, v = logical_kv(dd.meta, dd.layer, r)
+        p = int(dd.prefix[r])
+        args = (k[:p].double().cpu().numpy(), v[:p].double().cpu().numpy(),
+                dd.q[:, r].double().cpu().numpy(), dd.k_new[:, r].double().cpu().numpy(),
+                dd.v_new[:, r].double().cpu().numpy(), dd.probs[r].cpu().numpy(),
+                dd.uniforms[:, r].cpu().numpy(), scale)
+        t0 = time.perf_counter()
+        oracle.draft.draft_request(*args)
+        t_total += time.perf_counter() - t0
+        done += 1
+        if t_total >= budget_s and done >= 2:
+            break
+    return {"value": round(done / t_total, 3), "unit": "requests/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} of {cfg.bs} requests of the {cfg.name} draft stage "
+                      f"({dd.steps} steps: append, attention, sampling), {t_total:.1f} s of "
+                      f"fp64 numpy"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -320,6 +491,9 @@ def main():
         return
     if args.h2d:
         h2d_bench(args)
+        return
+    if args.draft:
+        draft_bench(args)
         return
     import torch
     import paper_2609_29364_amd as nsd

@@ -9,6 +9,9 @@
  *                         queries of every request over the paged KV cache
  *   nsd_spec_accept       acceptance of proposals and residual resampling
  *
+ * The draft stage before it (Eq. 1) is single-query nsd_verify_attention
+ * steps, each after nsd_kv_append of the processed token, and nsd_sample.
+ *
  * nsd_gather_verify_attention does the first two in one pass (each staged
  * byte read once); nsd_copy_plan moves KV between a pinned host arena and a
  * device bank (the host-side source of the preparation).
@@ -305,6 +308,30 @@ nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
                            const int32_t* draft_tokens, const float* uniforms,
                            const int32_t* q_indptr, int32_t bs, int32_t vocab, int32_t max_k,
                            int32_t* accepted_len, int32_t* out_tokens, void* stream);
+
+/*
+ * Draw one token per row by inverse CDF: the sampling of a draft step,
+ * x_i ~ q_i (the draft stage precedes verification, Eq. 1; speculative
+ * decoding as in the works cited in Sections 1 and 2).
+ *
+ * Row r is w = probs[r * row_stride .. r * row_stride + vocab) (nonnegative
+ * weights, any total), its uniform uniforms[r] in [0,1).  The token is step 3
+ * of nsd_spec_accept on that row: y = min{t : C(t) > u_r * C(vocab-1)} over
+ * fp64 prefix sums in token order (the last token of positive weight if
+ * rounding leaves none; -1 if the row has no mass); it is written to
+ * out_tokens[r * out_stride].  With probs and out_tokens offset by step i and
+ * strides K * vocab and K, step i of a K-step chain reads the draft rows and
+ * writes the proposal tokens in the request-major layout nsd_spec_accept
+ * takes (q_draft row and draft_tokens entry r * K + i).
+ *
+ * probs : device fp32, 16-byte aligned; row_stride (elements) >= vocab and a
+ * multiple of 4.  uniforms : device fp32 [n_rows].  out_tokens : device int32,
+ * n_rows entries at stride out_stride >= 1.  vocab as in nsd_spec_accept.
+ * n_rows == 0 is a no-op.
+ */
+nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* uniforms,
+                      int32_t n_rows, int32_t vocab, int32_t* out_tokens, int32_t out_stride,
+                      void* stream);
 
 #ifdef __cplusplus
 }

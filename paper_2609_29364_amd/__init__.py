@@ -41,6 +41,7 @@ _SIGS = {
                                            _I32, _I32, _I32, _I32, _I32, _I32, _I32, _F32, _P,
                                            _P, _SZ, _P]),
     "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
+    "nsd_sample": (_I32, [_P, _I64, _P, _I32, _I32, _P, _I32, _P]),
     "nsd_copy_plan": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I32, _P]),
     "nsd_kv_append": (_I32, [_P, _P, _I64, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _I32, _I32,
                              _P]),
@@ -243,6 +244,31 @@ def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, acce
     return accepted_len, out_tokens
 
 
+def sample(probs, uniforms, out=None):
+    """One token per row by inverse CDF (the draft step's x_i ~ q_i).
+
+    probs: fp32 [n][V] on the GPU whose rows may be strided (unit stride within
+    a row, row stride a multiple of 4), e.g. step i of request-major draft rows
+    ``q_draft.view(bs, K, V)[:, i]``; uniforms: fp32 [n]; out: int32 [n],
+    possibly strided (e.g. ``draft_tokens.view(bs, K)[:, i]``).  Returns out."""
+    if probs.dtype != torch.float32 or not probs.is_cuda or probs.dim() != 2:
+        raise TypeError("probs must be a 2-d fp32 GPU tensor")
+    n, vocab = probs.shape
+    if (n > 1 and probs.stride(0) < vocab) or (vocab > 1 and probs.stride(1) != 1):
+        raise ValueError("probs rows must be unit-stride and not overlap")
+    _dev(uniforms, torch.float32, "uniforms")
+    if uniforms.numel() != n:
+        raise ValueError("uniforms must have one entry per row")
+    if out is None:
+        out = torch.empty(n, dtype=torch.int32, device=probs.device)
+    if out.dtype != torch.int32 or not out.is_cuda or out.dim() != 1 or out.numel() != n:
+        raise ValueError("out must be int32 [n] on the GPU")
+    _check("sample", lib().nsd_sample(
+        _ptr(probs), probs.stride(0) if n > 1 else vocab, _ptr(uniforms), n, vocab, _ptr(out),
+        max(1, out.stride(0)), _stream(probs)))
+    return out
+
+
 COPY_H2D, COPY_D2H = 1, 2
 DEFAULT_CHUNK = 32 << 20   # bytes per DMA submission
 
@@ -324,4 +350,4 @@ def kv_writeback(k_pool, v_pool, host_k, host_v, src_ids, dst_ids):
 __all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
            "new_workspace", "gather_verify_attention", "copy_plan", "COPY_H2D", "COPY_D2H",
            "DEFAULT_CHUNK", "kv_append", "commit_lengths", "host_alias", "kv_writeback",
-           "spec_accept", "NsdError", "BLOCK_SIZE", "LIB_PATH"]
+           "spec_accept", "sample", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

@@ -16,6 +16,9 @@
 // 4. Wave 0 re-reads that one chunk, scans it across lanes and picks the
 //    first token t with w(t) > 0 whose running prefix exceeds tau.
 // Total traffic: each needed row once plus one 1 KiB chunk.
+//
+// The same kernel, instantiated with SAMPLE, draws x ~ w from one row per
+// workgroup (the draft step's sampling x_i ~ q_i): steps 2-4 with w the row.
 #include "nsd_internal.h"
 
 namespace {
@@ -57,24 +60,32 @@ __device__ inline void weights4(const float4& pv, const float4& qv, bool resid, 
   }
 }
 
+// SAMPLE: plain draw x ~ w from row r (w = the row itself, steps 2-4 only):
+// row r at p_target + r * row_stride, uniform uniforms[r], token written to
+// out_tokens[r * out_stride]; q_indptr, q_draft, draft_tokens and
+// accepted_len are not used.
+template <bool SAMPLE>
 __global__ __launch_bounds__(kThreads) void spec_accept_kernel(
     const float* __restrict__ p_target, const float* __restrict__ q_draft,
     const int32_t* __restrict__ draft_tokens, const float* __restrict__ uniforms,
     const int32_t* __restrict__ q_indptr, int32_t vocab, int32_t max_k,
-    int32_t* __restrict__ accepted_len, int32_t* __restrict__ out_tokens) {
+    int32_t* __restrict__ accepted_len, int32_t* __restrict__ out_tokens, int64_t row_stride,
+    int32_t out_stride) {
   extern __shared__ double lds[];   // [nchunk] chunk sums, then [nchunk] exclusive prefixes
   __shared__ int s_n;
   __shared__ double s_total;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = blockIdx.x;
-  const int a = q_indptr[r];
-  const int k = max(0, min(q_indptr[r + 1] - a - 1, max_k));
+  const int a = SAMPLE ? r : q_indptr[r];
+  const int k = SAMPLE ? 0 : max(0, min(q_indptr[r + 1] - a - 1, max_k));
   const int nchunk = (vocab + kChunk - 1) / kChunk;
   double* csum = lds;
   double* cpre = lds + nchunk;
 
-  if (wave == 0) {
+  if (SAMPLE) {
+    if (threadIdx.x == 0) s_n = 0;
+  } else if (wave == 0) {
     bool ok = true;
     if (lane < k) {
       const int x = draft_tokens[a - r + lane];
@@ -92,7 +103,8 @@ __global__ __launch_bounds__(kThreads) void spec_accept_kernel(
   __syncthreads();
   const int n = s_n;
   bool resid = n < k;
-  const float* prow = p_target + (int64_t)(a + n) * vocab;
+  const float* prow = SAMPLE ? p_target + (int64_t)r * row_stride
+                            : p_target + (int64_t)(a + n) * vocab;
   const float* qrow = resid ? q_draft + (int64_t)(a - r + n) * vocab : prow;
 
   for (int attempt = 0; attempt < 2; ++attempt) {
@@ -197,6 +209,10 @@ __global__ __launch_bounds__(kThreads) void spec_accept_kernel(
       }
     }
   }
+  if (SAMPLE) {
+    if (lane == 0) out_tokens[(int64_t)r * out_stride] = y;
+    return;
+  }
   if (lane <= k) {
     int tok = -1;
     if (lane < n) tok = draft_tokens[a - r + lane];
@@ -229,8 +245,32 @@ extern "C" nsd_status nsd_spec_accept(const float* p_target, const float* q_draf
   const int nchunk = (vocab + kChunk - 1) / kChunk;
   const size_t lds = 2 * (size_t)nchunk * sizeof(double);
   clear_stale_error();
-  hipLaunchKernelGGL(spec_accept_kernel, dim3(bs), dim3(kThreads), lds, (hipStream_t)stream,
-                     p_target, q_draft, draft_tokens, uniforms, q_indptr, vocab, max_k,
-                     accepted_len, out_tokens);
+  hipLaunchKernelGGL(spec_accept_kernel<false>, dim3(bs), dim3(kThreads), lds,
+                     (hipStream_t)stream, p_target, q_draft, draft_tokens, uniforms, q_indptr,
+                     vocab, max_k, accepted_len, out_tokens, (int64_t)vocab, 1);
   return check_launch("spec_accept");
+}
+
+extern "C" nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* uniforms,
+                                 int32_t n_rows, int32_t vocab, int32_t* out_tokens,
+                                 int32_t out_stride, void* stream) {
+  using namespace nsd;
+  if (n_rows < 0) return fail(NSD_ERR_SHAPE, "sample: n_rows < 0");
+  if (vocab < 4 || vocab > kMaxVocab || vocab % 4)
+    return fail(NSD_ERR_UNSUPPORTED, "sample: vocab must be a multiple of 4 in [4, %d] (got %d)",
+                kMaxVocab, vocab);
+  if (row_stride < vocab || row_stride % 4)
+    return fail(NSD_ERR_SHAPE, "sample: row_stride must be a multiple of 4 and >= vocab "
+                "(got %lld)", (long long)row_stride);
+  if (out_stride < 1) return fail(NSD_ERR_SHAPE, "sample: out_stride < 1");
+  if (n_rows == 0) return NSD_OK;
+  if (!probs || !uniforms || !out_tokens) return fail(NSD_ERR_NULL, "sample: NULL pointer argument");
+  if ((uintptr_t)probs & 15) return fail(NSD_ERR_SHAPE, "sample: probs must be 16-byte aligned");
+  const int nchunk = (vocab + kChunk - 1) / kChunk;
+  const size_t lds = 2 * (size_t)nchunk * sizeof(double);
+  clear_stale_error();
+  hipLaunchKernelGGL(spec_accept_kernel<true>, dim3(n_rows), dim3(kThreads), lds,
+                     (hipStream_t)stream, probs, nullptr, nullptr, uniforms, nullptr, vocab, 0,
+                     nullptr, out_tokens, row_stride, out_stride);
+  return check_launch("sample");
 }

@@ -5,9 +5,12 @@ append of the window's new K/V rows (when given) and verification attention,
 then spec_accept and the commit of accepted lengths.  The preparation runs
 either as its own gather before the layers, or fused into each layer's
 attention pass (the layer's staged tiles are read once, used and written to
-the pool)."""
+the pool).
+
+The draft stage that precedes it (Eq. 1) is composed the same way: K steps of
+append, single-query attention and sampling."""
 from . import (kv_gather, verify_attention, gather_verify_attention, spec_accept, kv_append,
-               commit_lengths)
+               commit_lengths, sample)
 
 
 def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_table, seq_lens,
@@ -32,10 +35,7 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
     elif window_kv is not None:
         # fused preparation: an arriving request's blocks are still in the staging
         # bank, so its window rows go there and the pass moves whole blocks to the pool
-        import torch
-        arriving = stage_table[:, :1] >= 0
-        pool_table = torch.where(arriving, torch.full_like(block_table, -1), block_table)
-        stage_rows = torch.where(arriving, stage_table, torch.full_like(stage_table, -1))
+        pool_table, stage_rows = _fused_tables(block_table, stage_table)
     outs = []
     for layer in range(k_pool.shape[0]):
         o = None if out is None else out[layer]
@@ -63,3 +63,57 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
         if committed is not None:
             commit_lengths(seq_lens, q_indptr, acc, out=committed)
     return outs if out is None else out, acc, tok
+
+
+def _fused_tables(block_table, stage_table):
+    """Append tables for the fused preparation: arriving requests (staging id in
+    entry 0) write into their staged blocks, resident ones into the pool."""
+    import torch
+    arriving = stage_table[:, :1] >= 0
+    pool_table = torch.where(arriving, torch.full_like(block_table, -1), block_table)
+    stage_rows = torch.where(arriving, stage_table, torch.full_like(stage_table, -1))
+    return pool_table, stage_rows
+
+
+def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, lens, q_indptr,
+                max_seq_len, k_stage=None, v_stage=None, src_ids=None, dst_ids=None,
+                stage_table=None, tokens=None, out=None, workspace=None, scale=None):
+    """K draft steps of one layer on one stream; returns (out, tokens).
+
+    Step i processes one token per request (the anchor, then proposal i-1): it
+    appends that token's K/V rows k_new[i], v_new[i] ([bs][Hkv][D]) at
+    position lens[i][r] - 1, attends with q[i] ([bs][Hq][D]) over positions
+    0 .. lens[i][r] - 1 into out[i], and draws proposal i from the draft rows
+    probs[:, i] with uniforms[i] into tokens[:, i].
+
+    probs: fp32 [bs][K][V] and tokens: int32 [bs][K] are request-major, the
+    q_draft / draft_tokens layout spec_accept takes; uniforms: fp32 [K][bs];
+    lens: int32 [K][bs] (step i: the step-0 lengths plus i); q_indptr: int32
+    [bs+1] = 0, 1, .., bs.  Arriving requests are prepared before step 0, by
+    the (src_ids, dst_ids) gather from the staging planes, or with
+    ``stage_table`` fused into step 0's attention pass (their step-0 rows are
+    appended into the staged blocks, which the pass moves to the pool)."""
+    import torch
+    n_steps, bs = lens.shape
+    if tokens is None:
+        tokens = torch.empty((bs, n_steps), dtype=torch.int32, device=probs.device)
+    if out is None:
+        out = torch.empty_like(q)
+    if stage_table is None:
+        if src_ids is not None and src_ids.numel():
+            kv_gather(k_stage, v_stage, k_pool, v_pool, src_ids, dst_ids)
+    else:
+        pool_table, stage_rows = _fused_tables(block_table, stage_table)
+    for i in range(n_steps):
+        if stage_table is not None and i == 0:
+            kv_append(k_pool, v_pool, k_new[i], v_new[i], pool_table, lens[i], q_indptr)
+            kv_append(k_stage, v_stage, k_new[i], v_new[i], stage_rows, lens[i], q_indptr)
+            gather_verify_attention(q[i], k_pool, v_pool, k_stage, v_stage, block_table,
+                                    stage_table, lens[i], q_indptr, 1, max_seq_len, scale=scale,
+                                    out=out[i], workspace=workspace)
+        else:
+            kv_append(k_pool, v_pool, k_new[i], v_new[i], block_table, lens[i], q_indptr)
+            verify_attention(q[i], k_pool, v_pool, block_table, lens[i], q_indptr, 1,
+                             max_seq_len, scale=scale, out=out[i], workspace=workspace)
+        sample(probs[:, i], uniforms[i], out=tokens[:, i])
+    return out, tokens

@@ -69,3 +69,29 @@ def check_accept(p, q, x, u, q_indptr, acc_gpu, tok_gpu, requests=None):
                 f"request {r}: token {yg} vs {yr} away from a CDF boundary"
             near += 1
     return near
+
+
+def check_samples(rows, u, got):
+    """Inverse-CDF draws against oracle.draft.sample: equal except within
+    CDF_BOUNDARY of a CDF boundary; a token of zero weight is never drawn.
+    rows: [n][V] host array, u: [n], got: [n] ints.  Returns the number of
+    boundary cases."""
+    rows = np.asarray(rows)
+    ref = oracle.draft.sample(rows, u)
+    near = 0
+    for i in range(len(rows)):
+        g, e = int(got[i]), int(ref[i])
+        if e < 0:
+            assert g == -1, f"row {i}: drew {g} from a row without mass"
+            continue
+        w = rows[i].astype(np.float64)
+        assert 0 <= g < len(w) and w[g] > 0, f"row {i}: token {g} has no weight"
+        if g != e:
+            c = np.cumsum(w)
+            lo, hi = min(g, e), max(g, e)
+            ui = float(u[i])
+            assert abs(c[lo] / c[-1] - ui) <= CDF_BOUNDARY and \
+                abs(c[hi - 1] / c[-1] - ui) <= CDF_BOUNDARY, \
+                f"row {i}: token {g} vs {e} away from a CDF boundary"
+            near += 1
+    return near

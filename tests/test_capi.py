@@ -92,6 +92,18 @@ def test_accept_validation(lib):
     assert f(None, None, None, None, None, 4, 1000, 4, None, None, None) == 1
 
 
+def test_sample_validation(lib):
+    f = lib.nsd_sample
+    assert f(None, 1000, None, 4, 1001, None, 1, None) == 3                # vocab % 4
+    assert f(None, 996, None, 4, 1000, None, 1, None) == 2                 # row_stride < vocab
+    assert f(None, 1002, None, 4, 1000, None, 1, None) == 2                # row_stride % 4
+    assert f(None, 1000, None, 4, 1000, None, 0, None) == 2                # out_stride
+    assert f(None, 1000, None, -1, 1000, None, 1, None) == 2
+    assert f(None, 1000, None, 0, 1000, None, 1, None) == 0
+    assert f(None, 1000, None, 4, 1000, None, 1, None) == 1
+    assert f(8, 1000, 8, 4, 1000, 8, 1, None) == 2 and b"aligned" in lib.nsd_last_error()
+
+
 def test_copy_plan_validation(lib):
     f = lib.nsd_copy_plan
     plan = (ctypes.c_int64 * 6)(0, 0, 64, 64, 64, 64)

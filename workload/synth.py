@@ -37,6 +37,7 @@ from .layout import BLOCK_SIZE, k_block_shape, v_block_shape, logical_kv_from_bl
 S_CTX, S_ARRIVE, S_POOL_PERM, S_STAGE_PERM, S_DEPTH = 1, 2, 3, 4, 5
 S_Q, S_K, S_V, S_P_LOGITS, S_Q_LOGITS, S_GUMBEL, S_UNIFORM = 6, 7, 8, 9, 10, 11, 12
 S_K_STAGE, S_V_STAGE = 13, 14
+S_DRAFT_Q, S_DRAFT_K, S_DRAFT_V, S_DRAFT_LOGITS, S_DRAFT_U = 15, 16, 17, 18, 19
 
 _CHUNK = 1 << 26
 
@@ -301,3 +302,72 @@ def make_hostkv(cfg: RoundConfig, meta: RoundMeta, layer: LayerData, headroom_to
             hk[extent[r]:extent[r] + n] = src_k[ids]
             hv[extent[r]:extent[r] + n] = src_v[ids]
     return HostKV(hk, hv, extent, cap)
+
+
+@dataclass
+class DraftData:
+    """Inputs of a K-step draft stage over one layer.
+
+    Request r enters with P_r = L_r - 1 tokens in its cache (L_r drawn as for a
+    round, the anchor included); step i processes the token at position P_r + i.
+    The block tables cover the last step's length P_r + K, and every slot at or
+    past P_r holds NaN until a step appends it."""
+    meta: RoundMeta             # seq_lens = P_r + K (tables sized for the last step), one query each
+    layer: LayerData            # pools and staging planes (layer.q is not used)
+    lens: torch.Tensor          # int32 [K][bs], step i's length P_r + i + 1
+    q: torch.Tensor             # bf16 [K][bs][Hq][D]
+    k_new: torch.Tensor         # bf16 [K][bs][Hkv][D]
+    v_new: torch.Tensor         # bf16 [K][bs][Hkv][D]
+    probs: torch.Tensor         # fp32 [bs][K][V], draft row of step i at [r][i]
+    uniforms: torch.Tensor      # fp32 [K][bs]
+
+    @property
+    def steps(self): return self.lens.shape[0]
+
+    @property
+    def prefix(self): return self.meta.seq_lens - self.steps   # P_r
+
+
+def _poison_positions(k, v, table, rows, pos):
+    """NaN into slot pos % 16 of block table[row][pos // 16] for each (row, pos)."""
+    if len(rows) == 0:
+        return
+    blk = torch.as_tensor(table[rows, pos // BLOCK_SIZE], dtype=torch.long, device=k.device)
+    slot = torch.as_tensor(pos % BLOCK_SIZE, dtype=torch.long, device=k.device)
+    k[blk, :, :, slot, :] = float("nan")
+    v[blk, :, :, slot] = float("nan")
+
+
+def make_draft(cfg: RoundConfig, steps: int, vocab: int, device) -> DraftData:
+    """Draw a draft stage of ``steps`` proposals per request: contexts, the
+    arriving set and block layout as for a round of ``cfg`` (one query per
+    request), per-step queries and new K/V rows N(0, 1) in bf16, draft rows
+    fp32(softmax_fp64(N(0, 2^2))) over ``vocab`` tokens, uniforms on the 2^-24
+    grid."""
+    if steps < 1:
+        raise ValueError("a draft stage has at least one step")
+    L = _np_rng(cfg.seed, S_CTX).integers(cfg.ctx_lo, cfg.ctx_hi + 1, size=cfg.bs)
+    meta = make_meta(cfg, seq_lens=L - 1 + steps, depth=np.zeros(cfg.bs, dtype=np.int32))
+    layer = make_layer(cfg, meta, 0, device)
+    # the cache holds P_r tokens; the positions the steps append are not there yet
+    prefix = meta.seq_lens - steps
+    rows = np.repeat(np.arange(cfg.bs), steps)
+    pos = (prefix[rows] + np.tile(np.arange(steps), cfg.bs)).astype(np.int64)
+    arr = meta.arriving[rows]
+    _poison_positions(layer.k_pool, layer.v_pool, meta.block_table, rows[~arr], pos[~arr])
+    _poison_positions(layer.k_stage, layer.v_stage, meta.stage_table, rows[arr], pos[arr])
+    lens = torch.as_tensor((prefix[None, :] + 1 + np.arange(steps)[:, None]).astype(np.int32),
+                           device=device)
+    bf = torch.bfloat16
+    hq, hkv, d = cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    q = torch.empty((steps, cfg.bs, hq, d), dtype=bf, device=device)
+    kn = torch.empty((steps, cfg.bs, hkv, d), dtype=bf, device=device)
+    vn = torch.empty((steps, cfg.bs, hkv, d), dtype=bf, device=device)
+    _fill_normal(q, _torch_gen(cfg.seed, S_DRAFT_Q, 0, device))
+    _fill_normal(kn, _torch_gen(cfg.seed, S_DRAFT_K, 0, device))
+    _fill_normal(vn, _torch_gen(cfg.seed, S_DRAFT_V, 0, device))
+    probs = torch.empty((cfg.bs, steps, vocab), dtype=torch.float32, device=device)
+    _softmax_rows(probs.view(-1, vocab), _torch_gen(cfg.seed, S_DRAFT_LOGITS, 0, device), 2.0)
+    ug = _torch_gen(cfg.seed, S_DRAFT_U, 0, device)
+    u = torch.randint(0, 1 << 24, (steps, cfg.bs), generator=ug, device=device, dtype=torch.int64)
+    return DraftData(meta, layer, lens, q, kn, vn, probs, u.to(torch.float32) * (2.0 ** -24))
