@@ -331,7 +331,7 @@ def draft_bench(args):
     the proposal."""
     import torch
     import paper_2609_29364_amd as nsd
-    from paper_2609_29364_amd.round import draft_stage
+    from paper_2609_29364_amd.round import draft_stage, fused_tables
     from workload import CONFIGS, make_draft
 
     dev = torch.device("cuda:0")
@@ -343,8 +343,7 @@ def draft_bench(args):
     i32 = lambda a: torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32, device=dev)
     bt, qi = i32(meta.block_table), i32(np.arange(cfg.bs + 1))
     st, src, dst = i32(meta.stage_table), i32(meta.src_ids), i32(meta.dst_ids)
-    pool_table = torch.where(st[:, :1] >= 0, torch.full_like(bt, -1), bt)
-    stage_rows = torch.where(st[:, :1] >= 0, st, torch.full_like(st, -1))
+    pool_table, stage_rows = fused_tables(bt, st)
     max_len = int(meta.seq_lens.max())
     ws = nsd.new_workspace(nsd.verify_attention_workspace_size(
         cfg.bs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 1, max_len), dev)
@@ -379,7 +378,8 @@ def draft_bench(args):
     def library_stage():
         draft_stage(kp, vp, dd.q, dd.k_new, dd.v_new, dd.probs, dd.uniforms, bt, dd.lens, qi,
                     max_len, k_stage=ks, v_stage=vs, stage_table=None if args.unfused else st,
-                    src_ids=src, dst_ids=dst, tokens=tok, out=out, workspace=ws)
+                    src_ids=src, dst_ids=dst, tokens=tok, out=out, workspace=ws,
+                    append_tables=(pool_table, stage_rows))
 
     # the timed region: the library's draft stage, back to back
     for _ in range(args.warmup):

@@ -15,7 +15,8 @@ from . import (kv_gather, verify_attention, gather_verify_attention, spec_accept
 
 def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_table, seq_lens,
                  q_indptr, max_q_per_seq, max_seq_len, accept=None, out=None, workspace=None,
-                 scale=None, stage_table=None, window_kv=None, committed=None):
+                 scale=None, stage_table=None, window_kv=None, committed=None,
+                 append_tables=None):
     """Run the round; returns (out, accepted_len, out_tokens).
 
     Pools and staging planes are stacked over layers ([layers][blocks][...]);
@@ -27,15 +28,17 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
     draft_tokens, uniforms, max_k).  ``window_kv`` is None (the pools already
     hold the window's K/V) or per-layer (k_new, v_new) rows [total_q][Hkv][D]
     appended before that layer's attention (into the staging bank for arriving
-    requests of the fused path, whose blocks the pass then moves to the pool).  With acceptance and a
-    ``committed`` int32 [bs] tensor, the committed lengths are written there.
+    requests of the fused path, whose blocks the pass then moves to the pool;
+    ``append_tables`` = fused_tables(block_table, stage_table), if given).  With
+    acceptance and a ``committed`` int32 [bs] tensor, the committed lengths are
+    written there.
     """
     if stage_table is None:
         kv_gather(k_stage, v_stage, k_pool, v_pool, src_ids, dst_ids)
     elif window_kv is not None:
         # fused preparation: an arriving request's blocks are still in the staging
         # bank, so its window rows go there and the pass moves whole blocks to the pool
-        pool_table, stage_rows = _fused_tables(block_table, stage_table)
+        pool_table, stage_rows = append_tables or fused_tables(block_table, stage_table)
     outs = []
     for layer in range(k_pool.shape[0]):
         o = None if out is None else out[layer]
@@ -65,9 +68,11 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
     return outs if out is None else out, acc, tok
 
 
-def _fused_tables(block_table, stage_table):
-    """Append tables for the fused preparation: arriving requests (staging id in
-    entry 0) write into their staged blocks, resident ones into the pool."""
+def fused_tables(block_table, stage_table):
+    """Append tables for the fused preparation, (pool_table, stage_rows): arriving
+    requests (staging id in entry 0) write into their staged blocks, resident
+    ones into the pool.  Batch metadata: build once per batch and pass as
+    ``append_tables``."""
     import torch
     arriving = stage_table[:, :1] >= 0
     pool_table = torch.where(arriving, torch.full_like(block_table, -1), block_table)
@@ -77,7 +82,8 @@ def _fused_tables(block_table, stage_table):
 
 def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, lens, q_indptr,
                 max_seq_len, k_stage=None, v_stage=None, src_ids=None, dst_ids=None,
-                stage_table=None, tokens=None, out=None, workspace=None, scale=None):
+                stage_table=None, tokens=None, out=None, workspace=None, scale=None,
+                append_tables=None):
     """K draft steps of one layer on one stream; returns (out, tokens).
 
     Step i processes one token per request (the anchor, then proposal i-1): it
@@ -92,7 +98,8 @@ def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, l
     [bs+1] = 0, 1, .., bs.  Arriving requests are prepared before step 0, by
     the (src_ids, dst_ids) gather from the staging planes, or with
     ``stage_table`` fused into step 0's attention pass (their step-0 rows are
-    appended into the staged blocks, which the pass moves to the pool)."""
+    appended into the staged blocks, which the pass moves to the pool;
+    ``append_tables`` = fused_tables(block_table, stage_table), if given)."""
     import torch
     n_steps, bs = lens.shape
     if tokens is None:
@@ -103,7 +110,7 @@ def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, l
         if src_ids is not None and src_ids.numel():
             kv_gather(k_stage, v_stage, k_pool, v_pool, src_ids, dst_ids)
     else:
-        pool_table, stage_rows = _fused_tables(block_table, stage_table)
+        pool_table, stage_rows = append_tables or fused_tables(block_table, stage_table)
     for i in range(n_steps):
         if stage_table is not None and i == 0:
             kv_append(k_pool, v_pool, k_new[i], v_new[i], pool_table, lens[i], q_indptr)
