@@ -16,6 +16,9 @@ Plain, slow, fp64 numpy restatements of what the round computes:
 * ``draft``     -- the draft stage before verification (Eq. 1): K single-query
                    decode steps over the draft cache and inverse-CDF sampling
                    of each proposal.
+* ``schedule``  -- worker-triggered batch reconstruction (Algorithm 1,
+                   Eqs. 4-8) and the profiling-driven discrete-event
+                   simulator with ideal migration (Appendix H).
 
 Only the test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library
@@ -26,6 +29,6 @@ Every function is pinned by ``tests/test_oracle_*.py`` against a library
 routine, closed forms, invariants or a sampling theorem; none is "parity
 unpinned".
 """
-from . import gather, attention, accept, commit, draft
+from . import gather, attention, accept, commit, draft, schedule
 
-__all__ = ["gather", "attention", "accept", "commit", "draft"]
+__all__ = ["gather", "attention", "accept", "commit", "draft", "schedule"]
