@@ -333,6 +333,101 @@ nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* unifo
                       int32_t n_rows, int32_t vocab, int32_t* out_tokens, int32_t out_stride,
                       void* stream);
 
+/*
+ * Worker-triggered batch reconstruction: one scheduling opportunity (host
+ * code; no GPU involved).
+ *
+ * Passage: Section 4, Algorithm 1 and Eqs. 4-8 (predicted predecessor
+ * completion, batch KV-ready and start times, service-admission bound,
+ * admissibility); Appendix F.2 (capacity fit, each request individually).
+ *
+ * Candidate i is request ids[i] with available predecessor completion time
+ * e_tilde[i] and KV-ready time k_hat[i] on the worker, which is available at
+ * a_hat.  S({r}) = max(a_hat, e~_r, k^_r); d^_r = max(e~_r + g, S({r})) + delta.
+ * Candidates with blocks[i] > block_cap or tokens[i] > token_cap are dropped;
+ * the rest are ranked by (d^_r, S({r}), id) ascending (earliest admission
+ * bound first: a longer wait gives an earlier bound), the first b_max of them
+ * are scanned once in that order and r joins if the batch stays admissible:
+ * its blocks and tokens within the capacities and
+ * max(a_hat, max e~, max k^) <= min d^ over the batch.
+ * blocks / tokens may be NULL (all zero).  ids must be distinct; times may be
+ * +/-infinity but not NaN; g, delta >= 0 (delta may be +infinity).
+ * Out: batch[0 .. *batch_len) in admission order (batch holds b_max entries),
+ * *batch_start = S(B) (NaN when the batch is empty).  n == 0 gives an empty
+ * batch.  All pointers host memory.
+ */
+nsd_status nsd_reconstruct(const int32_t* ids, const double* e_tilde, const double* k_hat,
+                           const int64_t* blocks, const int64_t* tokens, int32_t n, double a_hat,
+                           int64_t block_cap, int64_t token_cap, int32_t b_max, double g,
+                           double delta, int32_t* batch, int32_t* batch_len,
+                           double* batch_start);
+
+/*
+ * Profiling-driven discrete-event simulation of the two worker pools with
+ * ideal migration (host code; no GPU involved).
+ *
+ * Passage: Appendix H (simulation methodology: virtual clock, all transitions
+ * at one time applied before scheduling, compute and Prepare opportunities per
+ * worker, zero migration latency; all requests start after prefill at t = 0
+ * and run a fixed number of rounds; Eqs. H.1 and H.2 and the request-round
+ * rate over a window); Eq. 1 (draft before target in every round); Appendix F
+ * (standby-bank planning, early planning with predicted predecessor ends,
+ * Prepare then Run on InputReady, KVReady and WorkerReady).
+ *
+ * Workers 0 .. n_draft-1 serve the draft stage, the next n_target the target
+ * stage.  Stage s takes phi_s(b) for a batch of b requests, with SM activity
+ * sm_s(b), both interpolated linearly over the table's batch sizes (constant
+ * beyond its ends).  At every virtual time: completions; then, until nothing
+ * changes, each worker without a prepared batch (index order) reconstructs
+ * one (nsd_reconstruct with a_hat = the end of its running batch or now,
+ * k^ = now, no capacity limit, stage s's b_max, g, delta) over the requests
+ * whose next stage is s and whose latest other-stage instance is running
+ * (e~ = its predicted end) or done, and each idle worker whose prepared batch
+ * has every predecessor output published starts it.
+ *
+ * phi_d / phi_t : host double [3][n] = batch sizes (ascending), stage times
+ *                 (> 0), SM activity, for the draft and target stages.
+ * metrics : U = sum_j tau_j sm_j / ((n_draft + n_target) (w1 - w0)),
+ *           S = sum_j tau_j b_j / (n_requests (w1 - w0)), round_rate =
+ *           request-level target rounds ending in (w0, w1] / (w1 - w0),
+ *           finished requests, batches started; tau_j = overlap of batch j
+ *           with [w0, w1].
+ * trace / members (optional, NULL with capacity 0): batch j's record and its
+ *           request ids at members[first .. first + size), in start order.
+ *           If either buffer is too small the simulation still completes,
+ *           metrics are valid, *n_trace / *n_members give the sizes needed
+ *           and NSD_ERR_WORKSPACE is returned.
+ * The run stops when no batch is running, or once virtual time passes t_stop
+ * (INFINITY: run to completion).
+ */
+typedef struct {
+  int32_t n_draft, n_target;  /* workers per pool, >= 1 each */
+  int32_t n_requests, rounds; /* requests, speculative rounds per request */
+  int32_t b_max[2];           /* [draft, target] maximum batch sizes */
+  double g[2];                /* target service intervals g_s, >= 0 */
+  double delta[2];            /* slacks Delta_s, >= 0 */
+  double window[2];           /* measurement window [w0, w1], w0 < w1 */
+  double t_stop;
+} nsd_sim_config;
+
+typedef struct {
+  double U, S, round_rate;
+  int64_t finished, batches;
+} nsd_sim_metrics;
+
+typedef struct {
+  int32_t stage;   /* 0 draft, 1 target */
+  int32_t worker;  /* index within its pool */
+  int32_t size;
+  int64_t first;   /* offset of its members */
+  double start, end;
+} nsd_sim_batch;
+
+nsd_status nsd_simulate(const nsd_sim_config* cfg, const double* phi_d, int32_t n_phi_d,
+                        const double* phi_t, int32_t n_phi_t, nsd_sim_metrics* metrics,
+                        nsd_sim_batch* trace, int64_t trace_cap, int32_t* members,
+                        int64_t members_cap, int64_t* n_trace, int64_t* n_members);
+
 #ifdef __cplusplus
 }
 #endif

@@ -42,6 +42,9 @@ _SIGS = {
                                            _P, _SZ, _P]),
     "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
     "nsd_sample": (_I32, [_P, _I64, _P, _I32, _I32, _P, _I32, _P]),
+    "nsd_reconstruct": (_I32, [_P, _P, _P, _P, _P, _I32, ctypes.c_double, _I64, _I64, _I32,
+                               ctypes.c_double, ctypes.c_double, _P, _P, _P]),
+    "nsd_simulate": (_I32, [_P, _P, _I32, _P, _I32, _P, _P, _I64, _P, _I64, _P, _P]),
     "nsd_copy_plan": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I32, _P]),
     "nsd_kv_append": (_I32, [_P, _P, _I64, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _I32, _I32,
                              _P]),

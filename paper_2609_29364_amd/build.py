@@ -10,7 +10,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(HERE, "libnebulasd.so")
 SOURCES = ["status.cpp", "kv_gather.hip", "verify_attention.hip", "spec_accept.hip",
-           "copy_plan.cpp", "kv_commit.hip"]
+           "copy_plan.cpp", "kv_commit.hip", "scheduler.cpp"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
