@@ -45,6 +45,13 @@ def parse():
     ap.add_argument("--draft", action="store_true",
                     help="time the draft stage instead (Eq. 1): --draft-steps single-query "
                          "decode steps (append, attention, sampling) on draft_decode")
+    ap.add_argument("--phi", action="store_true",
+                    help="profile the stage-time tables the scheduler uses (phi_s of Eq. 4): "
+                         "one target round layer (fused pass + acceptance) and one 4-step draft "
+                         "stage layer over a range of batch sizes; prints one JSON line")
+    ap.add_argument("--schedule", action="store_true",
+                    help="host-side scheduler (no GPU): batch-reconstruction decision latency "
+                         "and a pool-scale simulation, the library against the oracle")
     ap.add_argument("--draft-steps", type=int, default=4)
     ap.add_argument("--draft-vocab", type=int, default=151936)
     args = ap.parse_args()
@@ -361,7 +368,8 @@ def draft_bench(args):
             if ev: ev[1 + 3 * i].record(stream)
             if i == 0 and not args.unfused:
                 nsd.kv_append(kp, vp, dd.k_new[0], dd.v_new[0], pool_table, dd.lens[0], qi)
-                nsd.kv_append(ks, vs, dd.k_new[0], dd.v_new[0], stage_rows, dd.lens[0], qi)
+                if ks.numel():
+                    nsd.kv_append(ks, vs, dd.k_new[0], dd.v_new[0], stage_rows, dd.lens[0], qi)
             else:
                 nsd.kv_append(kp, vp, dd.k_new[i], dd.v_new[i], bt, dd.lens[i], qi)
             if ev: ev[2 + 3 * i].record(stream)
@@ -449,6 +457,174 @@ def draft_bench(args):
     print(json.dumps(res), flush=True)
 
 
+def phi_bench(args):
+    """Stage times of our kernels against batch size (one layer): the target
+    round on verify_8b-shaped requests (contexts U[1024, 4096], K = 4, 30 %
+    arriving; fused preparation + attention, then acceptance) and the draft
+    stage on draft_decode-shaped requests (contexts U[512, 2048], 25 %
+    arriving, --draft-steps proposals over --draft-vocab tokens)."""
+    import dataclasses
+    import torch
+    import paper_2609_29364_amd as nsd
+    from paper_2609_29364_amd.round import draft_stage, fused_tables
+    from workload import CONFIGS, make_meta, make_layer, make_accept, make_draft
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    i32 = lambda a: torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def timed(fn, n):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    target = {"sizes": [], "ms": []}
+    for b in (1, 4, 8, 16, 32, 64, 128, 256, 512):
+        cfg = dataclasses.replace(CONFIGS["verify_8b"], bs=b, n_arriving=int(round(0.3 * b)))
+        meta = make_meta(cfg)
+        lay = make_layer(cfg, meta, 0, dev)
+        acc = make_accept(cfg, meta, dev)
+        bt, st, sl, qi = (i32(meta.block_table), i32(meta.stage_table), i32(meta.seq_lens),
+                          i32(meta.q_indptr))
+        ws = nsd.new_workspace(nsd.verify_attention_workspace_size(
+            b, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, meta.max_q, meta.max_seq_len), dev)
+        out = torch.empty_like(lay.q)
+        al = torch.empty(b, dtype=torch.int32, device=dev)
+        tk = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
+
+        def round_():
+            nsd.gather_verify_attention(lay.q, lay.k_pool, lay.v_pool, lay.k_stage, lay.v_stage,
+                                        bt, st, sl, qi, meta.max_q, meta.max_seq_len, out=out,
+                                        workspace=ws)
+            nsd.spec_accept(acc.p_target, acc.q_draft, acc.draft_tokens, acc.uniforms, qi,
+                            cfg.k_hi, accepted_len=al, out_tokens=tk)
+        target["sizes"].append(b)
+        target["ms"].append(round(timed(round_, max(5, args.steps // 2)), 5))
+        del meta, lay, acc, ws, out
+        torch.cuda.empty_cache()
+    draft = {"sizes": [], "ms": []}
+    for b in (1, 16, 64, 128, 256, 512, 1024):
+        cfg = dataclasses.replace(CONFIGS["draft_decode"], bs=b, n_arriving=b // 4)
+        dd = make_draft(cfg, args.draft_steps, args.draft_vocab, dev)
+        meta, lay = dd.meta, dd.layer
+        bt, st = i32(meta.block_table), i32(meta.stage_table)
+        qi = i32(np.arange(b + 1))
+        tables = fused_tables(bt, st)
+        max_len = int(meta.seq_lens.max())
+        ws = nsd.new_workspace(nsd.verify_attention_workspace_size(
+            b, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 1, max_len), dev)
+        out = torch.empty_like(dd.q)
+        tok = torch.empty((b, args.draft_steps), dtype=torch.int32, device=dev)
+
+        def stage_():
+            draft_stage(lay.k_pool, lay.v_pool, dd.q, dd.k_new, dd.v_new, dd.probs, dd.uniforms,
+                        bt, dd.lens, qi, max_len, k_stage=lay.k_stage, v_stage=lay.v_stage,
+                        stage_table=st, tokens=tok, out=out, workspace=ws, append_tables=tables)
+        draft["sizes"].append(b)
+        draft["ms"].append(round(timed(stage_, max(5, args.steps // 2)), 5))
+        del dd, meta, lay, ws, out
+        torch.cuda.empty_cache()
+    print(json.dumps({"mode": "phi", "layers": 1, "draft_steps": args.draft_steps,
+                      "draft_vocab": args.draft_vocab,
+                      "target": target | {"workload": "verify_8b shapes, bs varied"},
+                      "draft": draft | {"workload": "draft_decode shapes, bs varied"}}),
+          flush=True)
+
+
+# Stage profiles printed in Appendix C (batch-size profiling): one draft forward
+# takes about 16 ms at batch 1 and 18 ms at 512, 38.6 ms at 1024, with SM
+# activity 9.1 %, 86.8 % and 95.1 %; target verification at depth 4 reaches SM
+# activity 74.1 % at 1 request, 87.5 % at 32, 93.2 % at 64 and 95.7 % at 128,
+# taking 28.8 ms at 32, 46.3 ms at 64 and 82.8 ms at 128 (below 32 the time is
+# taken as flat).  A draft stage is `depth` forwards.
+PAPER_PHI_DRAFT_FWD = ([1, 512, 1024], [0.016, 0.018, 0.0386], [0.091, 0.868, 0.951])
+PAPER_PHI_TARGET = ([1, 32, 64, 128], [0.0288, 0.0288, 0.0463, 0.0828],
+                    [0.741, 0.875, 0.932, 0.957])
+
+
+def schedule_bench(args):
+    """Host scheduler: one JSON line (no GPU).
+
+    * decision latency: one reconstruction over C candidates (predecessor ends
+      and KV-ready times uniform over 10 ms, worker free at 5 ms, g = 0, Delta =
+      30 ms), the library against the oracle;
+    * simulation (Appendix H): 6 draft + 32 target workers, 4096 requests, 32
+      rounds of depth 4, draft/target batch limits 512/32, window [1, 2.5] s,
+      with the stage profiles printed in Appendix C, and with our kernels' own
+      one-layer stage times (profiles/phi_tables.json, from bench.py --phi)."""
+    import paper_2609_29364_amd.schedule as sch
+    import oracle
+    rng = np.random.default_rng(0)
+    lat = []
+    for c, bmax in ((1024, 32), (16384, 32), (16384, 512)):
+        ids = np.arange(c, dtype=np.int32)
+        e = rng.uniform(0, 0.01, c)
+        k = rng.uniform(0, 0.01, c)
+        el, kl = e.tolist(), k.tolist()
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < 0.5:
+            sch.reconstruct(ids, e, k, a_hat=0.005, b_max=bmax, g=0.0, delta=0.03)
+            n += 1
+        t_lib = (time.perf_counter() - t0) / n
+        t0 = time.perf_counter()
+        m = 0
+        z = [0] * c
+        while time.perf_counter() - t0 < 1.0 or m == 0:
+            oracle.schedule.reconstruct(list(range(c)), el, kl, z, z, 0.005, 0, 0, bmax, 0.0, 0.03)
+            m += 1
+        t_or = (time.perf_counter() - t0) / m
+        lat.append({"candidates": c, "b_max": bmax, "lib_us": round(t_lib * 1e6, 2),
+                    "oracle_us": round(t_or * 1e6, 1)})
+    depth = 4
+    phi_d = (PAPER_PHI_DRAFT_FWD[0], [depth * x for x in PAPER_PHI_DRAFT_FWD[1]],
+             PAPER_PHI_DRAFT_FWD[2])
+    sims = []
+    setups = [("paper Appendix C profiles", phi_d, PAPER_PHI_TARGET, (1.0, 2.5))]
+    try:
+        tab = json.load(open(os.path.join(ROOT, "profiles", "phi_tables.json")))
+        # our kernels: one layer of each stage, full activity (every launch fills the chip)
+        kd = (tab["draft"]["sizes"], [x * 1e-3 for x in tab["draft"]["ms"]],
+              [1.0] * len(tab["draft"]["sizes"]))
+        kt = (tab["target"]["sizes"], [x * 1e-3 for x in tab["target"]["ms"]],
+              [1.0] * len(tab["target"]["sizes"]))
+        setups.append(("our kernels, one layer per stage", kd, kt, (0.02, 0.08)))
+    except (OSError, KeyError, ValueError):
+        pass
+    for name, pd, pt, window in setups:
+        t0 = time.perf_counter()
+        m, _ = sch.simulate(6, 32, 4096, 32, pd, pt, 512, 32, 0.0, 0.0, 0.03 * window[1] / 2.5,
+                            0.03 * window[1] / 2.5, window, trace=False)
+        wall = time.perf_counter() - t0
+        sims.append({"profiles": name, "window_s": list(window),
+                     "U": round(m["U"], 4), "S": round(m["S"], 4),
+                     "round_rate": round(m["round_rate"], 1), "batches": m["batches"],
+                     "wall_s": round(wall, 3), "batches_per_s": round(m["batches"] / wall, 1)})
+    # the oracle on the first simulation (same inputs): equal metrics, its time
+    t0 = time.perf_counter()
+    mo, _ = oracle.schedule.simulate(6, 32, 4096, 32, phi_d, PAPER_PHI_TARGET, 512, 32, 0.0,
+                                     0.0, 0.03, 0.03, (1.0, 2.5))
+    t_or = time.perf_counter() - t0
+    ml, _ = sch.simulate(6, 32, 4096, 32, phi_d, PAPER_PHI_TARGET, 512, 32, 0.0, 0.0, 0.03,
+                         0.03, (1.0, 2.5), trace=False)
+    res = {"mode": "schedule", "metric": "scheduling decision latency (us); simulated pool "
+           "metrics (Eqs. H.1, H.2)", "decision_latency": lat, "simulation": sims,
+           "oracle_metrics_equal": ml == mo,
+           "cpu_baseline": {"value": round(mo["batches"] / t_or, 1), "unit": "batches/s",
+                            "cores": 1, "kind": "oracle",
+                            "sample": f"the oracle simulator on the first simulation above "
+                                      f"({mo['batches']} batches), {t_or:.1f} s"}}
+    print(json.dumps(res), flush=True)
+
+
 def draft_cpu_baseline(cfg, dd, budget_s):
     """The draft-stage oracle, untuned, on a bounded sample of the requests."""
     import oracle
@@ -486,6 +662,9 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; use --gpus 1"}))
         sys.exit(2)
+    if args.schedule:
+        schedule_bench(args)
+        return
     if args.calibrate_copy:
         calibrate_copy()
         return
@@ -494,6 +673,9 @@ def main():
         return
     if args.draft:
         draft_bench(args)
+        return
+    if args.phi:
+        phi_bench(args)
         return
     import torch
     import paper_2609_29364_amd as nsd

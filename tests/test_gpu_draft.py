@@ -121,7 +121,9 @@ def _check_stage(dd, out, tok, requests):
                    num_q_heads=16, num_kv_heads=8, head_dim=128, pool_blocks=None), 7),
     (custom_config(seed=52, bs=5, ctx_lo=30, ctx_hi=33, k_lo=0, k_hi=0, n_arriving=5,
                    pool_blocks=None), 16),
-], ids=["tiny_k4", "c2heads_k7", "all_arriving_k16"])
+    (custom_config(seed=54, bs=3, ctx_lo=5, ctx_hi=40, k_lo=0, k_hi=0, n_arriving=0,
+                   pool_blocks=None), 3),
+], ids=["tiny_k4", "c2heads_k7", "all_arriving_k16", "none_arriving_k3"])
 def test_draft_stage_matches_oracle(device, cfg, steps, fused):
     dd = make_draft(cfg, steps, 1000, device)
     out, tok = _run_stage(dd, device, fused)

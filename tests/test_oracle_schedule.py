@@ -164,3 +164,17 @@ def test_trace_invariants(seed):
         assert [s for s, _, _ in stages] == [0, 1] * rounds
         assert all(stages[i][2] <= stages[i + 1][1] for i in range(len(stages) - 1))
     assert 0.0 <= m["U"] <= 1.0 and 0.0 <= m["S"] <= 1.0
+
+
+def test_scaling_pools_and_requests_together_keeps_the_operating_point():
+    # Appendix H: with the draft-target ratio and the requests per worker fixed, the
+    # idealized simulator keeps U and S and scales the round rate with the pool
+    phi_d = ([1, 512, 1024], [0.064, 0.072, 0.1544], [0.091, 0.868, 0.951])
+    phi_t = ([1, 32, 64, 128], [0.0288, 0.0288, 0.0463, 0.0828], [0.741, 0.875, 0.932, 0.957])
+    base, _ = simulate(1, 4, 150, 6, phi_d, phi_t, 64, 16, 0.0, 0.0, 0.03, 0.03, (0.1, 0.4))
+    for k in (2, 3):
+        m, _ = simulate(k, 4 * k, 150 * k, 6, phi_d, phi_t, 64, 16, 0.0, 0.0, 0.03, 0.03,
+                        (0.1, 0.4))
+        assert math.isclose(m["U"], base["U"], rel_tol=1e-12)
+        assert math.isclose(m["S"], base["S"], rel_tol=1e-12)
+        assert math.isclose(m["round_rate"], k * base["round_rate"], rel_tol=1e-12)
