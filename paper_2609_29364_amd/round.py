@@ -48,7 +48,9 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
                 kv_append(k_pool[layer], v_pool[layer], kn, vn, block_table, seq_lens, q_indptr)
             else:
                 kv_append(k_pool[layer], v_pool[layer], kn, vn, pool_table, seq_lens, q_indptr)
-                kv_append(k_stage[layer], v_stage[layer], kn, vn, stage_rows, seq_lens, q_indptr)
+                if k_stage[layer].numel():
+                    kv_append(k_stage[layer], v_stage[layer], kn, vn, stage_rows, seq_lens,
+                              q_indptr)
         if stage_table is None:
             outs.append(verify_attention(q[layer], k_pool[layer], v_pool[layer], block_table,
                                          seq_lens, q_indptr, max_q_per_seq, max_seq_len,
@@ -114,7 +116,8 @@ def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, l
     for i in range(n_steps):
         if stage_table is not None and i == 0:
             kv_append(k_pool, v_pool, k_new[i], v_new[i], pool_table, lens[i], q_indptr)
-            kv_append(k_stage, v_stage, k_new[i], v_new[i], stage_rows, lens[i], q_indptr)
+            if k_stage.numel():      # no staged blocks when nothing arrives
+                kv_append(k_stage, v_stage, k_new[i], v_new[i], stage_rows, lens[i], q_indptr)
             gather_verify_attention(q[i], k_pool, v_pool, k_stage, v_stage, block_table,
                                     stage_table, lens[i], q_indptr, 1, max_seq_len, scale=scale,
                                     out=out[i], workspace=workspace)
