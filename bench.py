@@ -209,6 +209,8 @@ def h2d_bench(args):
         cfg.bs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, meta.max_q, meta.max_seq_len), dev)
     acc_len = torch.empty(cfg.bs, dtype=torch.int32, device=dev)
     toks = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
+    acc_ws = torch.empty(max(1, nsd.accept_workspace_size(cfg.bs, max(cfg.vocab, 4))),
+                         dtype=torch.uint8, device=dev)
     comp = torch.cuda.current_stream(dev)
 
     def round_(i):
@@ -217,7 +219,8 @@ def h2d_bench(args):
                                     meta.max_q, meta.max_seq_len, out=out, workspace=ws)
         if acc_in is not None:
             nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
-                            acc_in.uniforms, qi, cfg.k_hi, accepted_len=acc_len, out_tokens=toks)
+                            acc_in.uniforms, qi, cfg.k_hi, accepted_len=acc_len, out_tokens=toks,
+                            workspace=acc_ws)
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
     # H2D alone (both banks filled, so every round below reads valid staging)
@@ -356,6 +359,7 @@ def draft_bench(args):
         cfg.bs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 1, max_len), dev)
     out = torch.empty_like(dd.q)
     tok = torch.empty((cfg.bs, K), dtype=torch.int32, device=dev)
+    sw = torch.empty(nsd.accept_workspace_size(cfg.bs, V), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     kp, vp, ks, vs = layer.k_pool, layer.v_pool, layer.k_stage, layer.v_stage
 
@@ -380,14 +384,14 @@ def draft_bench(args):
                 nsd.verify_attention(dd.q[i], kp, vp, bt, dd.lens[i], qi, 1, max_len, out=out[i],
                                      workspace=ws)
             if ev: ev[3 + 3 * i].record(stream)
-            nsd.sample(dd.probs[:, i], dd.uniforms[i], out=tok[:, i])
+            nsd.sample(dd.probs[:, i], dd.uniforms[i], out=tok[:, i], workspace=sw)
         if ev: ev[1 + 3 * K].record(stream)
 
     def library_stage():
         draft_stage(kp, vp, dd.q, dd.k_new, dd.v_new, dd.probs, dd.uniforms, bt, dd.lens, qi,
                     max_len, k_stage=ks, v_stage=vs, stage_table=None if args.unfused else st,
                     src_ids=src, dst_ids=dst, tokens=tok, out=out, workspace=ws,
-                    append_tables=(pool_table, stage_rows))
+                    append_tables=(pool_table, stage_rows), sample_workspace=sw)
 
     # the timed region: the library's draft stage, back to back
     for _ in range(args.warmup):
@@ -499,13 +503,14 @@ def phi_bench(args):
         out = torch.empty_like(lay.q)
         al = torch.empty(b, dtype=torch.int32, device=dev)
         tk = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
+        aw = torch.empty(nsd.accept_workspace_size(b, cfg.vocab), dtype=torch.uint8, device=dev)
 
         def round_():
             nsd.gather_verify_attention(lay.q, lay.k_pool, lay.v_pool, lay.k_stage, lay.v_stage,
                                         bt, st, sl, qi, meta.max_q, meta.max_seq_len, out=out,
                                         workspace=ws)
             nsd.spec_accept(acc.p_target, acc.q_draft, acc.draft_tokens, acc.uniforms, qi,
-                            cfg.k_hi, accepted_len=al, out_tokens=tk)
+                            cfg.k_hi, accepted_len=al, out_tokens=tk, workspace=aw)
         target["sizes"].append(b)
         target["ms"].append(round(timed(round_, max(5, args.steps // 2)), 5))
         del meta, lay, acc, ws, out
@@ -523,11 +528,14 @@ def phi_bench(args):
             b, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 1, max_len), dev)
         out = torch.empty_like(dd.q)
         tok = torch.empty((b, args.draft_steps), dtype=torch.int32, device=dev)
+        sw = torch.empty(nsd.accept_workspace_size(b, args.draft_vocab), dtype=torch.uint8,
+                         device=dev)
 
         def stage_():
             draft_stage(lay.k_pool, lay.v_pool, dd.q, dd.k_new, dd.v_new, dd.probs, dd.uniforms,
                         bt, dd.lens, qi, max_len, k_stage=lay.k_stage, v_stage=lay.v_stage,
-                        stage_table=st, tokens=tok, out=out, workspace=ws, append_tables=tables)
+                        stage_table=st, tokens=tok, out=out, workspace=ws, append_tables=tables,
+                        sample_workspace=sw)
         draft["sizes"].append(b)
         draft["ms"].append(round(timed(stage_, max(5, args.steps // 2)), 5))
         del dd, meta, lay, ws, out
@@ -704,6 +712,8 @@ def main():
     ws = nsd.new_workspace(ws_n, dev)
     acc_len = torch.empty(cfg.bs, dtype=torch.int32, device=dev)
     toks = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
+    acc_ws = torch.empty(max(1, nsd.accept_workspace_size(cfg.bs, max(cfg.vocab, 4))),
+                         dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     def step(ev=None):
@@ -720,7 +730,8 @@ def main():
         if ev: ev[2].record(stream)
         if acc_in is not None:
             nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
-                            acc_in.uniforms, qi, cfg.k_hi, accepted_len=acc_len, out_tokens=toks)
+                            acc_in.uniforms, qi, cfg.k_hi, accepted_len=acc_len, out_tokens=toks,
+                            workspace=acc_ws)
         if ev: ev[3].record(stream)
 
     for _ in range(args.warmup):

@@ -301,13 +301,21 @@ nsd_status nsd_host_alias(const void* host, void** device_alias);
  * q_indptr : device, int32 [bs+1], q_indptr[0] = 0, 0 <= K_r <= max_k.
  * vocab : 4 <= vocab <= 2^19, vocab % 4 == 0; 0 <= max_k <= 63.
  * accepted_len : device, int32 [bs];  out_tokens : device, int32 [total_q].
- * Row bases must be 16-byte aligned (true for cudaMalloc'd/torch tensors).
- * q_draft and draft_tokens may be NULL when max_k == 0.  bs == 0 is a no-op.
+ * Row bases must be 16-byte aligned (true for hipMalloc'd/torch tensors).
+ * q_draft and draft_tokens may be NULL when max_k == 0.  bs <= 2^31 / 32;
+ * bs == 0 is a no-op.
+ * workspace : device, 8-byte aligned, at least
+ * nsd_spec_accept_workspace_size(bs, vocab) bytes, any contents (per-chunk
+ * sums of each request's weight row; the call writes all it reads); calls
+ * that overlap in time need separate workspaces.  Too small a workspace
+ * returns NSD_ERR_WORKSPACE.
  */
+size_t     nsd_spec_accept_workspace_size(int32_t rows, int32_t vocab);
 nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
                            const int32_t* draft_tokens, const float* uniforms,
                            const int32_t* q_indptr, int32_t bs, int32_t vocab, int32_t max_k,
-                           int32_t* accepted_len, int32_t* out_tokens, void* stream);
+                           int32_t* accepted_len, int32_t* out_tokens, void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /*
  * Draw one token per row by inverse CDF: the sampling of a draft step,
@@ -326,12 +334,14 @@ nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
  *
  * probs : device fp32, 16-byte aligned; row_stride (elements) >= vocab and a
  * multiple of 4.  uniforms : device fp32 [n_rows].  out_tokens : device int32,
- * n_rows entries at stride out_stride >= 1.  vocab as in nsd_spec_accept.
- * n_rows == 0 is a no-op.
+ * n_rows entries at stride out_stride >= 1.  vocab as in nsd_spec_accept;
+ * n_rows <= 2^31 / 32.  workspace as in nsd_spec_accept, of
+ * nsd_spec_accept_workspace_size(n_rows, vocab) bytes.  n_rows == 0 is a
+ * no-op.
  */
 nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* uniforms,
                       int32_t n_rows, int32_t vocab, int32_t* out_tokens, int32_t out_stride,
-                      void* stream);
+                      void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Worker-triggered batch reconstruction: one scheduling opportunity (host

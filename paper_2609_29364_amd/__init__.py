@@ -40,8 +40,9 @@ _SIGS = {
     "nsd_gather_verify_attention": (_I32, [_P, _P, _P, _I64, _P, _P, _I64, _P, _P, _I32, _P, _P,
                                            _I32, _I32, _I32, _I32, _I32, _I32, _I32, _F32, _P,
                                            _P, _SZ, _P]),
-    "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
-    "nsd_sample": (_I32, [_P, _I64, _P, _I32, _I32, _P, _I32, _P]),
+    "nsd_spec_accept_workspace_size": (_SZ, [_I32, _I32]),
+    "nsd_spec_accept": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _SZ, _P]),
+    "nsd_sample": (_I32, [_P, _I64, _P, _I32, _I32, _P, _I32, _P, _SZ, _P]),
     "nsd_reconstruct": (_I32, [_P, _P, _P, _P, _P, _I32, ctypes.c_double, _I64, _I64, _I32,
                                ctypes.c_double, ctypes.c_double, _P, _P, _P]),
     "nsd_simulate": (_I32, [_P, _P, _I32, _P, _I32, _P, _P, _I64, _P, _I64, _P, _P]),
@@ -219,9 +220,26 @@ def gather_verify_attention(q, k_cache, v_cache, k_stage, v_stage, block_table, 
     return out
 
 
+def accept_workspace_size(rows, vocab):
+    """Bytes of workspace spec_accept (rows = bs) or sample (rows = n_rows) needs."""
+    return lib().nsd_spec_accept_workspace_size(rows, vocab)
+
+
+def _accept_ws(workspace, rows, vocab, device):
+    need = accept_workspace_size(rows, vocab)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    if not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous GPU tensor")
+    return workspace, workspace.numel() * workspace.element_size()
+
+
 def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, accepted_len=None,
-                out_tokens=None):
-    """Acceptance + residual resampling; returns (accepted_len [bs], out_tokens [total_q]) int32."""
+                out_tokens=None, workspace=None):
+    """Acceptance + residual resampling; returns (accepted_len [bs], out_tokens [total_q]) int32.
+
+    workspace: a GPU tensor of at least accept_workspace_size(bs, vocab) bytes
+    (allocated per call when None)."""
     _dev(p_target, torch.float32, "p_target")
     _dev(uniforms, torch.float32, "uniforms")
     _dev(q_indptr, torch.int32, "q_indptr")
@@ -240,20 +258,23 @@ def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, acce
         out_tokens = torch.empty(total_q, dtype=torch.int32, device=p_target.device)
     _dev(accepted_len, torch.int32, "accepted_len")
     _dev(out_tokens, torch.int32, "out_tokens")
+    ws, ws_n = _accept_ws(workspace, bs, vocab, p_target.device)
     _check("spec_accept", lib().nsd_spec_accept(
         _ptr(p_target), _ptr(q_draft) if max_k > 0 else None,
         _ptr(draft_tokens) if max_k > 0 else None, _ptr(uniforms), _ptr(q_indptr), bs, vocab,
-        max_k, _ptr(accepted_len), _ptr(out_tokens), _stream(p_target)))
+        max_k, _ptr(accepted_len), _ptr(out_tokens), _ptr(ws), ws_n, _stream(p_target)))
     return accepted_len, out_tokens
 
 
-def sample(probs, uniforms, out=None):
+def sample(probs, uniforms, out=None, workspace=None):
     """One token per row by inverse CDF (the draft step's x_i ~ q_i).
 
     probs: fp32 [n][V] on the GPU whose rows may be strided (unit stride within
     a row, row stride a multiple of 4), e.g. step i of request-major draft rows
     ``q_draft.view(bs, K, V)[:, i]``; uniforms: fp32 [n]; out: int32 [n],
-    possibly strided (e.g. ``draft_tokens.view(bs, K)[:, i]``).  Returns out."""
+    possibly strided (e.g. ``draft_tokens.view(bs, K)[:, i]``); workspace: at
+    least accept_workspace_size(n, V) bytes (allocated per call when None).
+    Returns out."""
     if probs.dtype != torch.float32 or not probs.is_cuda or probs.dim() != 2:
         raise TypeError("probs must be a 2-d fp32 GPU tensor")
     n, vocab = probs.shape
@@ -266,9 +287,10 @@ def sample(probs, uniforms, out=None):
         out = torch.empty(n, dtype=torch.int32, device=probs.device)
     if out.dtype != torch.int32 or not out.is_cuda or out.dim() != 1 or out.numel() != n:
         raise ValueError("out must be int32 [n] on the GPU")
+    ws, ws_n = _accept_ws(workspace, n, vocab, probs.device)
     _check("sample", lib().nsd_sample(
         _ptr(probs), probs.stride(0) if n > 1 else vocab, _ptr(uniforms), n, vocab, _ptr(out),
-        max(1, out.stride(0)), _stream(probs)))
+        max(1, out.stride(0)), _ptr(ws), ws_n, _stream(probs)))
     return out
 
 
@@ -353,4 +375,4 @@ def kv_writeback(k_pool, v_pool, host_k, host_v, src_ids, dst_ids):
 __all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
            "new_workspace", "gather_verify_attention", "copy_plan", "COPY_H2D", "COPY_D2H",
            "DEFAULT_CHUNK", "kv_append", "commit_lengths", "host_alias", "kv_writeback",
-           "spec_accept", "sample", "NsdError", "BLOCK_SIZE", "LIB_PATH"]
+           "spec_accept", "accept_workspace_size", "sample", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

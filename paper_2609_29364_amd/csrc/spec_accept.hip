@@ -1,40 +1,60 @@
 // Speculative acceptance with residual resampling, the verification rule of
 // the speculative-decoding works the paper builds on (Leviathan et al. 2023;
-// Chen et al. 2023; cited in Sections 1 and 2).
+// Chen et al. 2023; cited in Sections 1 and 2); and plain inverse-CDF
+// sampling of one row (the draft step's x_i ~ q_i).
 //
-// One 1024-thread workgroup per request:
-// 1. Wave 0 evaluates the K_r acceptance tests u_i * q_i(x_i) <= p_i(x_i)
-//    exactly in fp64, one proposal per lane; a ballot gives the first
-//    rejection n.
-// 2. All 16 waves stream the weight row (max(0, p_n - q_n), or p_K) once in
-//    256-element chunks (one float4 per lane), reducing each chunk's fp64 sum
-//    with wave shuffles into LDS.  Loads for four chunks are issued before
-//    their arithmetic.
-// 3. Wave 0 scans the chunk sums (fp64 wave prefix scans with a carry) and
-//    finds, by ballot, the first chunk whose inclusive prefix exceeds
-//    tau = u_K * S.
-// 4. Wave 0 re-reads that one chunk, scans it across lanes and picks the
-//    first token t with w(t) > 0 whose running prefix exceeds tau.
-// Total traffic: each needed row once plus one 1 KiB chunk.
+// A request's weight row (max(0, p_n - q_n) after a rejection at n, or the
+// bonus row p_K) is 151936 floats in the workloads: streaming it is the whole
+// cost.  Two kernels:
 //
-// The same kernel, instantiated with SAMPLE, draws x ~ w from one row per
-// workgroup (the draft step's sampling x_i ~ q_i): steps 2-4 with w the row.
+// 1. row_sums_kernel, one 256-thread workgroup per (row, segment of 64
+//    chunks).  Every workgroup first evaluates the request's K acceptance
+//    tests u_i * q_i(x_i) <= p_i(x_i) exactly in fp64 (one proposal per lane;
+//    a ballot gives the first rejection n; redundant across a request's
+//    segments, a few scattered loads), then streams its segment of the weight row in 256-element chunks
+//    (one 16-byte load per lane, four chunks of loads in flight per wave,
+//    reduced together in one butterfly) and writes each chunk's fp64 sum to
+//    the workspace.  The row is spread over
+//    the whole chip instead of one workgroup per request.
+// 2. pick_kernel, one 256-thread workgroup per row: reads the row's chunk sums,
+//    scans them (a thread owns consecutive chunks; a block scan of the thread
+//    totals), finds the first chunk whose inclusive prefix exceeds
+//    tau = u_K * S, re-reads that one chunk and picks the first token t with
+//    w(t) > 0 whose running prefix exceeds tau.  A residual without mass (only
+//    possible through fp32 rounding) falls back to p_n, streamed here.
+// Traffic: each needed row once, plus the chunk sums (8 bytes per 1 KiB) and
+// one 1 KiB chunk per row.
 #include "nsd_internal.h"
 
 namespace {
 
-constexpr int kThreads = 1024;
-constexpr int kWaves = kThreads / 64;
-constexpr int kChunk = 256;       // weights per chunk: 64 lanes x float4
-constexpr int kUnroll = 4;
-constexpr int kMaxVocab = 1 << 19;
-constexpr int kMaxK = 63;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
 
-__device__ inline double wave_sum(double x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
-  return x;
-}
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kChunk = 256;       // weights per chunk: 64 lanes x 4
+constexpr int kUnroll = 4;
+constexpr int kSegChunks = kWaves * kUnroll * 4;   // chunks per row_sums workgroup
+constexpr int kMaxVocab = 1 << 19;
+constexpr int kMaxChunks = kMaxVocab / kChunk;
+constexpr int kMaxK = 63;
+constexpr int kMaxSegs = kMaxChunks / kSegChunks;
+constexpr int kMaxRows = 0x7fffffff / kMaxSegs;   // row_sums_kernel grid: segments x rows
+
+struct Args {
+  const float* p;              // target rows, or the rows to sample (SAMPLE)
+  const float* q;              // draft rows
+  const int32_t* x;            // proposal tokens
+  const float* u;              // uniforms
+  const int32_t* q_indptr;     // [rows + 1] (not SAMPLE)
+  int32_t vocab, max_k, nchunk;
+  int64_t row_stride;          // SAMPLE: elements between rows
+  int32_t out_stride;          // SAMPLE: entries between output tokens
+  double* ws_sum;              // [rows][nchunk]
+  int32_t* ws_n;               // [rows]
+  int32_t* accepted_len;
+  int32_t* out_tokens;
+};
 
 // Inclusive prefix sum across the wave (Hillis-Steele).
 __device__ inline double wave_incl_scan(double x, int lane) {
@@ -46,7 +66,7 @@ __device__ inline double wave_incl_scan(double x, int lane) {
   return x;
 }
 
-__device__ inline void weights4(const float4& pv, const float4& qv, bool resid, double w[4]) {
+__device__ inline void weights4(const f32x4& pv, const f32x4& qv, bool resid, double w[4]) {
   if (resid) {
     w[0] = fmax(0.0, (double)pv.x - (double)qv.x);
     w[1] = fmax(0.0, (double)pv.y - (double)qv.y);
@@ -60,177 +80,298 @@ __device__ inline void weights4(const float4& pv, const float4& qv, bool resid, 
   }
 }
 
-// SAMPLE: plain draw x ~ w from row r (w = the row itself, steps 2-4 only):
-// row r at p_target + r * row_stride, uniform uniforms[r], token written to
-// out_tokens[r * out_stride]; q_indptr, q_draft, draft_tokens and
-// accepted_len are not used.
+// Request r's first row a and clamped proposal count k; wave 0 evaluates the
+// acceptance tests and leaves the first rejection n in *s_n.
 template <bool SAMPLE>
-__global__ __launch_bounds__(kThreads) void spec_accept_kernel(
-    const float* __restrict__ p_target, const float* __restrict__ q_draft,
-    const int32_t* __restrict__ draft_tokens, const float* __restrict__ uniforms,
-    const int32_t* __restrict__ q_indptr, int32_t vocab, int32_t max_k,
-    int32_t* __restrict__ accepted_len, int32_t* __restrict__ out_tokens, int64_t row_stride,
-    int32_t out_stride) {
-  extern __shared__ double lds[];   // [nchunk] chunk sums, then [nchunk] exclusive prefixes
-  __shared__ int s_n;
-  __shared__ double s_total;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int r = blockIdx.x;
-  const int a = SAMPLE ? r : q_indptr[r];
-  const int k = SAMPLE ? 0 : max(0, min(q_indptr[r + 1] - a - 1, max_k));
-  const int nchunk = (vocab + kChunk - 1) / kChunk;
-  double* csum = lds;
-  double* cpre = lds + nchunk;
-
+__device__ inline void acceptance(const Args& A, int r, int lane, int wave, int& a, int& k,
+                                  int* s_n) {
   if (SAMPLE) {
-    if (threadIdx.x == 0) s_n = 0;
-  } else if (wave == 0) {
+    a = r;
+    k = 0;
+    return;
+  }
+  a = A.q_indptr[r];
+  k = max(0, min(A.q_indptr[r + 1] - a - 1, A.max_k));
+  if (wave == 0) {
     bool ok = true;
     if (lane < k) {
-      const int x = draft_tokens[a - r + lane];
-      if (x < 0 || x >= vocab) {
+      const int x = A.x[a - r + lane];
+      if (x < 0 || x >= A.vocab) {
         ok = false;
       } else {
-        const double uq = (double)uniforms[a + lane] *
-                          (double)q_draft[(int64_t)(a - r + lane) * vocab + x];
-        ok = uq <= (double)p_target[(int64_t)(a + lane) * vocab + x];
+        const double uq =
+            (double)A.u[a + lane] * (double)A.q[(int64_t)(a - r + lane) * A.vocab + x];
+        ok = uq <= (double)A.p[(int64_t)(a + lane) * A.vocab + x];
       }
     }
     const uint64_t rejected = __ballot(!ok);
-    if (lane == 0) s_n = rejected ? (__ffsll((unsigned long long)rejected) - 1) : k;
+    if (lane == 0) *s_n = rejected ? (__ffsll((unsigned long long)rejected) - 1) : k;
   }
+}
+
+template <bool SAMPLE>
+__device__ inline const float* row_p(const Args& A, int r, int a, int n) {
+  return SAMPLE ? A.p + (int64_t)r * A.row_stride : A.p + (int64_t)(a + n) * A.vocab;
+}
+
+// Sums of chunks [c_beg, c_end) of the weight row into dst[c].
+__device__ inline void chunk_sums(const float* prow, const float* qrow, bool resid, int vocab,
+                                  int c_beg, int c_end, int lane, int wave, double* dst) {
+  for (int c0 = c_beg + wave; c0 < c_end; c0 += kWaves * kUnroll) {
+    f32x4 pv[kUnroll], qv[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int c = c0 + u * kWaves;
+      const int idx = c * kChunk + lane * 4;
+      pv[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
+      qv[u] = pv[u];
+      if (c < c_end && idx < vocab) {
+        pv[u] = __builtin_nontemporal_load((const f32x4*)(prow + idx));
+        if (resid) qv[u] = __builtin_nontemporal_load((const f32x4*)(qrow + idx));
+      }
+    }
+    // the four chunk sums in one butterfly: halves of the lanes swap two
+    // chunks' values (xor 32), then one (xor 16), then 16-lane sums; lanes 0,
+    // 16, 32, 48 end with chunks 0, 1, 2, 3
+    double v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      double w[4];
+      weights4(pv[u], qv[u], resid, w);
+      v[u] = ((w[0] + w[1]) + w[2]) + w[3];
+    }
+    const bool h5 = lane & 32, h4 = lane & 16;
+    const double r0 = (h5 ? v[2] : v[0]) + __shfl_xor(h5 ? v[0] : v[2], 32);
+    const double r1 = (h5 ? v[3] : v[1]) + __shfl_xor(h5 ? v[1] : v[3], 32);
+    double s = (h4 ? r1 : r0) + __shfl_xor(h4 ? r0 : r1, 16);
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+    if ((lane & 15) == 0) {
+      const int c = c0 + ((h5 ? 2 : 0) + (h4 ? 1 : 0)) * kWaves;
+      if (c < c_end) dst[c] = s;
+    }
+  }
+}
+static_assert(kUnroll == 4, "the butterfly in chunk_sums reduces four chunks");
+
+template <bool SAMPLE>
+__global__ __launch_bounds__(kThreads) void row_sums_kernel(Args A) {
+  __shared__ int s_n;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nseg = (A.nchunk + kSegChunks - 1) / kSegChunks;
+  const int r = blockIdx.x / nseg;
+  const int seg = blockIdx.x - r * nseg;
+  int a, k;
+  acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n);
+  int n = 0;
+  if (!SAMPLE) {
+    __syncthreads();
+    n = s_n;
+  }
+  const bool resid = n < k;
+  const float* prow = row_p<SAMPLE>(A, r, a, n);
+  const float* qrow = resid ? A.q + (int64_t)(a - r + n) * A.vocab : prow;
+  const int c_beg = seg * kSegChunks;
+  const int c_end = min(A.nchunk, c_beg + kSegChunks);
+  chunk_sums(prow, qrow, resid, A.vocab, c_beg, c_end, lane, wave,
+             A.ws_sum + (int64_t)r * A.nchunk);
+  if (!SAMPLE && seg == 0 && threadIdx.x == 0) A.ws_n[r] = n;
+}
+
+// Exclusive block scan of one value per thread; *total gets the block's sum.
+__device__ inline double block_excl_scan(double v, int lane, int wave, double* s_w,
+                                         double* total) {
+  const double incl = wave_incl_scan(v, lane);
+  double excl = __shfl_up(incl, 1);
+  if (lane == 0) excl = 0.0;
+  if (lane == 63) s_w[wave] = incl;
   __syncthreads();
-  const int n = s_n;
-  bool resid = n < k;
-  const float* prow = SAMPLE ? p_target + (int64_t)r * row_stride
-                            : p_target + (int64_t)(a + n) * vocab;
-  const float* qrow = resid ? q_draft + (int64_t)(a - r + n) * vocab : prow;
+  double off = 0.0, all = 0.0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    if (w < wave) off += s_w[w];
+    all += s_w[w];
+  }
+  *total = all;
+  __syncthreads();
+  return off + excl;
+}
 
+template <bool SAMPLE>
+__global__ __launch_bounds__(kThreads) void pick_kernel(Args A) {
+  __shared__ double s_sum[kMaxChunks];
+  __shared__ double s_w[kWaves];
+  __shared__ double s_pre;
+  __shared__ int s_c;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int r = blockIdx.x;
+  const int nchunk = A.nchunk;
+  int a = r, k = 0, n = 0;
+  if (!SAMPLE) {
+    a = A.q_indptr[r];
+    k = max(0, min(A.q_indptr[r + 1] - a - 1, A.max_k));
+    n = min(max(A.ws_n[r], 0), k);
+  }
+  bool resid = n < k;
+  const float* prow = row_p<SAMPLE>(A, r, a, n);
+  const float* qrow = resid ? A.q + (int64_t)(a - r + n) * A.vocab : prow;
+  const double* sums = A.ws_sum + (int64_t)r * nchunk;
+  for (int c = tid; c < nchunk; c += kThreads) s_sum[c] = sums[c];
+  __syncthreads();
+
+  // thread tid owns chunks [c0, c1)
+  const int per = (nchunk + kThreads - 1) / kThreads;
+  const int c0 = min(nchunk, tid * per), c1 = min(nchunk, c0 + per);
+  double total = 0.0, pre = 0.0;
   for (int attempt = 0; attempt < 2; ++attempt) {
-    // 2. chunk sums
-    for (int c0 = wave; c0 < nchunk; c0 += kWaves * kUnroll) {
-      float4 pv[kUnroll], qv[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int c = c0 + u * kWaves;
-        const int idx = c * kChunk + lane * 4;
-        pv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-        qv[u] = pv[u];
-        if (c < nchunk && idx < vocab) {
-          pv[u] = *(const float4*)(prow + idx);
-          if (resid) qv[u] = *(const float4*)(qrow + idx);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int c = c0 + u * kWaves;
-        double w[4];
-        weights4(pv[u], qv[u], resid, w);
-        const double s = wave_sum(((w[0] + w[1]) + w[2]) + w[3]);
-        if (lane == 0 && c < nchunk) csum[c] = s;
-      }
-    }
-    __syncthreads();
-    // 3a. exclusive prefix of the chunk sums
-    if (wave == 0) {
-      double carry = 0.0;
-      for (int base = 0; base < nchunk; base += 64) {
-        const int c = base + lane;
-        const double v = c < nchunk ? csum[c] : 0.0;
-        const double incl = wave_incl_scan(v, lane);
-        double excl = __shfl_up(incl, 1);
-        if (lane == 0) excl = 0.0;
-        if (c < nchunk) cpre[c] = carry + excl;
-        carry += __shfl(incl, 63);
-      }
-      if (lane == 0) s_total = cpre[nchunk - 1] + csum[nchunk - 1];
-    }
-    __syncthreads();
-    if (s_total > 0.0 || !resid) break;
-    resid = false;   // residual without mass: draw from p_n itself
+    double local = 0.0;
+    for (int c = c0; c < c1; ++c) local += s_sum[c];
+    pre = block_excl_scan(local, lane, wave, s_w, &total);
+    if (total > 0.0 || !resid) break;
+    // residual without mass: draw from p_n itself
+    resid = false;
     qrow = prow;
+    chunk_sums(prow, qrow, false, A.vocab, 0, nchunk, lane, wave, s_sum);
     __syncthreads();
   }
-
-  if (wave != 0) return;
-  const double total = s_total;
-  const double tau = (double)uniforms[a + k] * total;
+  const double tau = (double)A.u[a + k] * total;
   int y = -1;
   if (total > 0.0) {
-    // 3b. first chunk whose inclusive prefix exceeds tau
-    int cstar = -1;
-    for (int base = 0; base < nchunk && cstar < 0; base += 64) {
-      const int c = base + lane;
-      const bool hit = c < nchunk && cpre[c] + csum[c] > tau;
-      const uint64_t m = __ballot(hit);
-      if (m) cstar = base + __ffsll((unsigned long long)m) - 1;
-    }
-    if (cstar < 0) {   // rounding: take the last chunk with mass
-      for (int base = ((nchunk - 1) / 64) * 64; base >= 0 && cstar < 0; base -= 64) {
-        const int c = base + lane;
-        const uint64_t m = __ballot(c < nchunk && csum[c] > 0.0);
-        if (m) cstar = base + 63 - __clzll((long long)m);
+    // the first chunk whose inclusive prefix exceeds tau, else the last with mass
+    if (tid == 0) s_c = 0x7fffffff;
+    __syncthreads();
+    double run = pre;
+    int found = -1;
+    double found_pre = 0.0;
+    for (int c = c0; c < c1; ++c) {
+      if (run + s_sum[c] > tau) {
+        found = c;
+        found_pre = run;
+        break;
       }
+      run += s_sum[c];
     }
-    // 4. scan inside the chosen chunk
-    if (cstar < 0) cstar = 0;   // unreachable when total > 0; keeps addresses in range
-    const int idx = cstar * kChunk + lane * 4;
-    float4 pv = make_float4(0.f, 0.f, 0.f, 0.f), qv = pv;
-    if (idx < vocab) {
-      pv = *(const float4*)(prow + idx);
-      if (resid) qv = *(const float4*)(qrow + idx);
+    if (found >= 0) atomicMin(&s_c, found);
+    __syncthreads();
+    if (found >= 0 && found == s_c) s_pre = found_pre;
+    if (s_c == 0x7fffffff) {
+      __syncthreads();
+      if (tid == 0) s_c = -1;
+      __syncthreads();
+      int last = -1;
+      double last_pre = 0.0, acc = pre;
+      for (int c = c0; c < c1; ++c) {
+        if (s_sum[c] > 0.0) {
+          last = c;
+          last_pre = acc;
+        }
+        acc += s_sum[c];
+      }
+      if (last >= 0) atomicMax(&s_c, last);
+      __syncthreads();
+      if (last >= 0 && last == s_c) s_pre = last_pre;
     }
-    double w[4];
-    weights4(pv, qv, resid, w);
-    const double ls = ((w[0] + w[1]) + w[2]) + w[3];
-    const double incl = wave_incl_scan(ls, lane);
-    double run = __shfl_up(incl, 1);
-    if (lane == 0) run = 0.0;
-    run += cpre[cstar];
-    int found = -1, last_pos = -1;
+    __syncthreads();
+    // scan inside the chosen chunk (wave 0)
+    if (wave == 0) {
+      const int cstar = max(s_c, 0);   // s_c >= 0 whenever total > 0
+      const int idx = cstar * kChunk + lane * 4;
+      f32x4 pv = (f32x4){0.f, 0.f, 0.f, 0.f}, qv = pv;
+      if (idx < A.vocab) {
+        pv = *(const f32x4*)(prow + idx);
+        if (resid) qv = *(const f32x4*)(qrow + idx);
+      }
+      double w[4];
+      weights4(pv, qv, resid, w);
+      const double ls = ((w[0] + w[1]) + w[2]) + w[3];
+      const double incl = wave_incl_scan(ls, lane);
+      double rr = __shfl_up(incl, 1);
+      if (lane == 0) rr = 0.0;
+      rr += s_pre;
+      int f = -1, last_pos = -1;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      run += w[e];
-      if (w[e] > 0.0) {
-        last_pos = e;
-        if (found < 0 && run > tau) found = e;
+      for (int e = 0; e < 4; ++e) {
+        rr += w[e];
+        if (w[e] > 0.0) {
+          last_pos = e;
+          if (f < 0 && rr > tau) f = e;
+        }
       }
-    }
-    const uint64_t fm = __ballot(found >= 0);
-    if (fm) {
-      const int fl = __ffsll((unsigned long long)fm) - 1;
-      y = cstar * kChunk + fl * 4 + __shfl(found, fl);
-    } else {
-      const uint64_t pm = __ballot(last_pos >= 0);
-      if (pm) {
-        const int pl = 63 - __clzll((long long)pm);
-        y = cstar * kChunk + pl * 4 + __shfl(last_pos, pl);
+      const uint64_t fm = __ballot(f >= 0);
+      if (fm) {
+        const int fl = __ffsll((unsigned long long)fm) - 1;
+        y = cstar * kChunk + fl * 4 + __shfl(f, fl);
+      } else {
+        const uint64_t pm = __ballot(last_pos >= 0);
+        if (pm) {
+          const int pl = 63 - __clzll((long long)pm);
+          y = cstar * kChunk + pl * 4 + __shfl(last_pos, pl);
+        }
       }
     }
   }
+  if (wave != 0) return;
   if (SAMPLE) {
-    if (lane == 0) out_tokens[(int64_t)r * out_stride] = y;
+    if (lane == 0) A.out_tokens[(int64_t)r * A.out_stride] = y;
     return;
   }
   if (lane <= k) {
     int tok = -1;
-    if (lane < n) tok = draft_tokens[a - r + lane];
+    if (lane < n) tok = A.x[a - r + lane];
     else if (lane == n) tok = y;
-    out_tokens[a + lane] = tok;
+    A.out_tokens[a + lane] = tok;
   }
-  if (lane == 0) accepted_len[r] = n;
+  if (lane == 0) A.accepted_len[r] = n;
+}
+
+int64_t sums_bytes(int64_t rows, int32_t vocab) {
+  const int64_t nchunk = (vocab + kChunk - 1) / kChunk;
+  return (rows * nchunk * 8 + 255) / 256 * 256;
+}
+
+nsd_status launch(bool sample, Args A, int32_t rows, void* workspace, size_t workspace_bytes,
+                  void* stream, const char* fn) {
+  using namespace nsd;
+  const size_t need = (size_t)(sums_bytes(rows, A.vocab) + (int64_t)rows * 4);
+  if (!workspace || workspace_bytes < need)
+    return fail(NSD_ERR_WORKSPACE, "%s: a workspace of %zu bytes is needed (got %zu)", fn, need,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace & 7)
+    return fail(NSD_ERR_SHAPE, "%s: the workspace must be 8-byte aligned", fn);
+  A.nchunk = (A.vocab + kChunk - 1) / kChunk;
+  A.ws_sum = (double*)workspace;
+  A.ws_n = (int32_t*)((char*)workspace + sums_bytes(rows, A.vocab));
+  const dim3 g1((uint32_t)((A.nchunk + kSegChunks - 1) / kSegChunks) * (uint32_t)rows);
+  clear_stale_error();
+  if (sample) {
+    hipLaunchKernelGGL(row_sums_kernel<true>, g1, dim3(kThreads), 0, (hipStream_t)stream, A);
+    hipLaunchKernelGGL(pick_kernel<true>, dim3(rows), dim3(kThreads), 0, (hipStream_t)stream, A);
+  } else {
+    hipLaunchKernelGGL(row_sums_kernel<false>, g1, dim3(kThreads), 0, (hipStream_t)stream, A);
+    hipLaunchKernelGGL(pick_kernel<false>, dim3(rows), dim3(kThreads), 0, (hipStream_t)stream, A);
+  }
+  return check_launch(fn);
 }
 
 }  // namespace
+
+extern "C" size_t nsd_spec_accept_workspace_size(int32_t rows, int32_t vocab) {
+  if (rows < 0 || vocab < 1 || vocab > kMaxVocab) return 0;
+  return (size_t)(sums_bytes(rows, vocab) + (int64_t)rows * 4);
+}
 
 extern "C" nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
                                       const int32_t* draft_tokens, const float* uniforms,
                                       const int32_t* q_indptr, int32_t bs, int32_t vocab,
                                       int32_t max_k, int32_t* accepted_len,
-                                      int32_t* out_tokens, void* stream) {
+                                      int32_t* out_tokens, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
   using namespace nsd;
-  if (bs < 0) return fail(NSD_ERR_SHAPE, "spec_accept: bs < 0");
+  if (bs < 0 || bs > kMaxRows)
+    return fail(NSD_ERR_SHAPE, "spec_accept: bs must be in [0, %d]", kMaxRows);
   if (vocab < 4 || vocab > kMaxVocab || vocab % 4)
     return fail(NSD_ERR_UNSUPPORTED, "spec_accept: vocab must be a multiple of 4 in [4, %d] "
                 "(got %d)", kMaxVocab, vocab);
@@ -242,20 +383,18 @@ extern "C" nsd_status nsd_spec_accept(const float* p_target, const float* q_draf
     return fail(NSD_ERR_NULL, "spec_accept: NULL pointer argument");
   if (((uintptr_t)p_target | (uintptr_t)(max_k > 0 ? q_draft : p_target)) & 15)
     return fail(NSD_ERR_SHAPE, "spec_accept: probability rows must be 16-byte aligned");
-  const int nchunk = (vocab + kChunk - 1) / kChunk;
-  const size_t lds = 2 * (size_t)nchunk * sizeof(double);
-  clear_stale_error();
-  hipLaunchKernelGGL(spec_accept_kernel<false>, dim3(bs), dim3(kThreads), lds,
-                     (hipStream_t)stream, p_target, q_draft, draft_tokens, uniforms, q_indptr,
-                     vocab, max_k, accepted_len, out_tokens, (int64_t)vocab, 1);
-  return check_launch("spec_accept");
+  Args A{p_target, q_draft, draft_tokens, uniforms, q_indptr, vocab, max_k, 0, (int64_t)vocab, 1,
+         nullptr, nullptr, accepted_len, out_tokens};
+  return launch(false, A, bs, workspace, workspace_bytes, stream, "spec_accept");
 }
 
 extern "C" nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* uniforms,
                                  int32_t n_rows, int32_t vocab, int32_t* out_tokens,
-                                 int32_t out_stride, void* stream) {
+                                 int32_t out_stride, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
   using namespace nsd;
-  if (n_rows < 0) return fail(NSD_ERR_SHAPE, "sample: n_rows < 0");
+  if (n_rows < 0 || n_rows > kMaxRows)
+    return fail(NSD_ERR_SHAPE, "sample: n_rows must be in [0, %d]", kMaxRows);
   if (vocab < 4 || vocab > kMaxVocab || vocab % 4)
     return fail(NSD_ERR_UNSUPPORTED, "sample: vocab must be a multiple of 4 in [4, %d] (got %d)",
                 kMaxVocab, vocab);
@@ -266,11 +405,7 @@ extern "C" nsd_status nsd_sample(const float* probs, int64_t row_stride, const f
   if (n_rows == 0) return NSD_OK;
   if (!probs || !uniforms || !out_tokens) return fail(NSD_ERR_NULL, "sample: NULL pointer argument");
   if ((uintptr_t)probs & 15) return fail(NSD_ERR_SHAPE, "sample: probs must be 16-byte aligned");
-  const int nchunk = (vocab + kChunk - 1) / kChunk;
-  const size_t lds = 2 * (size_t)nchunk * sizeof(double);
-  clear_stale_error();
-  hipLaunchKernelGGL(spec_accept_kernel<true>, dim3(n_rows), dim3(kThreads), lds,
-                     (hipStream_t)stream, probs, nullptr, nullptr, uniforms, nullptr, vocab, 0,
-                     nullptr, out_tokens, row_stride, out_stride);
-  return check_launch("sample");
+  Args A{probs, nullptr, nullptr, uniforms, nullptr, vocab, 0, 0, row_stride, out_stride,
+         nullptr, nullptr, nullptr, out_tokens};
+  return launch(true, A, n_rows, workspace, workspace_bytes, stream, "sample");
 }

@@ -10,13 +10,13 @@ the pool).
 The draft stage that precedes it (Eq. 1) is composed the same way: K steps of
 append, single-query attention and sampling."""
 from . import (kv_gather, verify_attention, gather_verify_attention, spec_accept, kv_append,
-               commit_lengths, sample)
+               commit_lengths, sample, accept_workspace_size)
 
 
 def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_table, seq_lens,
                  q_indptr, max_q_per_seq, max_seq_len, accept=None, out=None, workspace=None,
                  scale=None, stage_table=None, window_kv=None, committed=None,
-                 append_tables=None):
+                 append_tables=None, accept_workspace=None):
     """Run the round; returns (out, accepted_len, out_tokens).
 
     Pools and staging planes are stacked over layers ([layers][blocks][...]);
@@ -31,7 +31,7 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
     requests of the fused path, whose blocks the pass then moves to the pool;
     ``append_tables`` = fused_tables(block_table, stage_table), if given).  With
     acceptance and a ``committed`` int32 [bs] tensor, the committed lengths are
-    written there.
+    written there; ``accept_workspace`` is spec_accept's workspace.
     """
     if stage_table is None:
         kv_gather(k_stage, v_stage, k_pool, v_pool, src_ids, dst_ids)
@@ -64,7 +64,7 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
     acc = tok = None
     if accept is not None:
         p, qd, x, u, max_k = accept
-        acc, tok = spec_accept(p, qd, x, u, q_indptr, max_k)
+        acc, tok = spec_accept(p, qd, x, u, q_indptr, max_k, workspace=accept_workspace)
         if committed is not None:
             commit_lengths(seq_lens, q_indptr, acc, out=committed)
     return outs if out is None else out, acc, tok
@@ -85,7 +85,7 @@ def fused_tables(block_table, stage_table):
 def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, lens, q_indptr,
                 max_seq_len, k_stage=None, v_stage=None, src_ids=None, dst_ids=None,
                 stage_table=None, tokens=None, out=None, workspace=None, scale=None,
-                append_tables=None):
+                append_tables=None, sample_workspace=None):
     """K draft steps of one layer on one stream; returns (out, tokens).
 
     Step i processes one token per request (the anchor, then proposal i-1): it
@@ -101,9 +101,13 @@ def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, l
     the (src_ids, dst_ids) gather from the staging planes, or with
     ``stage_table`` fused into step 0's attention pass (their step-0 rows are
     appended into the staged blocks, which the pass moves to the pool;
-    ``append_tables`` = fused_tables(block_table, stage_table), if given)."""
+    ``append_tables`` = fused_tables(block_table, stage_table), if given).
+    ``sample_workspace``: accept_workspace_size(bs, V) bytes, one for all steps."""
     import torch
     n_steps, bs = lens.shape
+    if sample_workspace is None:
+        sample_workspace = torch.empty(accept_workspace_size(bs, probs.shape[-1]),
+                                       dtype=torch.uint8, device=probs.device)
     if tokens is None:
         tokens = torch.empty((bs, n_steps), dtype=torch.int32, device=probs.device)
     if out is None:
@@ -125,5 +129,5 @@ def draft_stage(k_pool, v_pool, q, k_new, v_new, probs, uniforms, block_table, l
             kv_append(k_pool, v_pool, k_new[i], v_new[i], block_table, lens[i], q_indptr)
             verify_attention(q[i], k_pool, v_pool, block_table, lens[i], q_indptr, 1,
                              max_seq_len, scale=scale, out=out[i], workspace=workspace)
-        sample(probs[:, i], uniforms[i], out=tokens[:, i])
+        sample(probs[:, i], uniforms[i], out=tokens[:, i], workspace=sample_workspace)
     return out, tokens

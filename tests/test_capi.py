@@ -85,23 +85,34 @@ def test_attention_workspace_check(lib):
 
 def test_accept_validation(lib):
     f = lib.nsd_spec_accept
-    assert f(None, None, None, None, None, 4, 1001, 4, None, None, None) == 3   # vocab % 4
-    assert f(None, None, None, None, None, 4, 1 << 20, 4, None, None, None) == 3
-    assert f(None, None, None, None, None, 4, 1000, 64, None, None, None) == 3
-    assert f(None, None, None, None, None, 0, 1000, 4, None, None, None) == 0
-    assert f(None, None, None, None, None, 4, 1000, 4, None, None, None) == 1
+    z = (None, 0, None)
+    assert f(None, None, None, None, None, 4, 1001, 4, None, None, *z) == 3   # vocab % 4
+    assert f(None, None, None, None, None, 4, 1 << 20, 4, None, None, *z) == 3
+    assert f(None, None, None, None, None, 4, 1000, 64, None, None, *z) == 3
+    assert f(None, None, None, None, None, 1 << 30, 1000, 4, None, None, *z) == 2
+    assert f(None, None, None, None, None, 0, 1000, 4, None, None, *z) == 0
+    assert f(None, None, None, None, None, 4, 1000, 4, None, None, *z) == 1
+    size = lib.nsd_spec_accept_workspace_size
+    assert size(256, 151936) == ((256 * 594 * 8 + 255) // 256) * 256 + 256 * 4
+    assert size(-1, 1000) == 0
+    # rows and probabilities present, workspace too small: refused before any launch
+    fake = 1 << 20
+    st = f(fake, fake, fake, fake, fake, 4, 1000, 4, fake, fake, fake, 16, None)
+    assert st == 4 and b"workspace" in lib.nsd_last_error()
 
 
 def test_sample_validation(lib):
     f = lib.nsd_sample
-    assert f(None, 1000, None, 4, 1001, None, 1, None) == 3                # vocab % 4
-    assert f(None, 996, None, 4, 1000, None, 1, None) == 2                 # row_stride < vocab
-    assert f(None, 1002, None, 4, 1000, None, 1, None) == 2                # row_stride % 4
-    assert f(None, 1000, None, 4, 1000, None, 0, None) == 2                # out_stride
-    assert f(None, 1000, None, -1, 1000, None, 1, None) == 2
-    assert f(None, 1000, None, 0, 1000, None, 1, None) == 0
-    assert f(None, 1000, None, 4, 1000, None, 1, None) == 1
-    assert f(8, 1000, 8, 4, 1000, 8, 1, None) == 2 and b"aligned" in lib.nsd_last_error()
+    z = (None, 0, None)
+    assert f(None, 1000, None, 4, 1001, None, 1, *z) == 3                # vocab % 4
+    assert f(None, 996, None, 4, 1000, None, 1, *z) == 2                 # row_stride < vocab
+    assert f(None, 1002, None, 4, 1000, None, 1, *z) == 2                # row_stride % 4
+    assert f(None, 1000, None, 4, 1000, None, 0, *z) == 2                # out_stride
+    assert f(None, 1000, None, -1, 1000, None, 1, *z) == 2
+    assert f(None, 1000, None, 0, 1000, None, 1, *z) == 0
+    assert f(None, 1000, None, 4, 1000, None, 1, *z) == 1
+    assert f(8, 1000, 8, 4, 1000, 8, 1, *z) == 2 and b"aligned" in lib.nsd_last_error()
+    assert f(16, 1000, 16, 4, 1000, 16, 1, *z) == 4                      # no workspace
 
 
 def test_copy_plan_validation(lib):

@@ -22,7 +22,7 @@ def _grid(g, shape):
     return (torch.randint(0, 1 << 24, shape, generator=g) * 2.0**-24).to(torch.float32)
 
 
-@pytest.mark.parametrize("vocab", [4, 1000, 4096, 151936])
+@pytest.mark.parametrize("vocab", [4, 1000, 4096, 16388, 151936, 1 << 19])
 def test_sample_matches_oracle(device, vocab):
     g = torch.Generator().manual_seed(vocab)
     n = 64

@@ -372,6 +372,32 @@ def test_accept_special_cases(device):
     check_accept(p, q, x, u, q_indptr, acc, tok)
 
 
+def test_accept_workspace_contents_do_not_matter(device):
+    # the chunk sums are written before they are read: a workspace full of NaN
+    # bytes, then reused across calls of different sizes, gives the same result
+    rng = np.random.default_rng(5)
+    out = []
+    for depth, vocab in (([3, 0, 5, 1], 16388), ([2] * 9, 1000), ([3, 0, 5, 1], 16388)):
+        q_indptr, tq, bs = _batch(depth)
+        p = _probs(rng, tq, vocab)
+        q = _probs(rng, tq - bs, vocab)
+        x = rng.integers(0, vocab, tq - bs).astype(np.int32)
+        u = (rng.integers(0, 1 << 24, tq) * 2.0**-24).astype(np.float32)
+        out.append((p, q, x, u, q_indptr, max(depth)))
+    ws = torch.full((nsd.accept_workspace_size(9, 16388),), 0xFF, dtype=torch.uint8,
+                    device=device)
+    t = lambda a, dt: torch.as_tensor(np.ascontiguousarray(a), dtype=dt, device=device)
+    for p, q, x, u, q_indptr, mk in out:
+        acc, tok = nsd.spec_accept(t(p, torch.float32), t(q, torch.float32), t(x, torch.int32),
+                                   t(u, torch.float32), t(q_indptr, torch.int32), mk,
+                                   workspace=ws)
+        torch.cuda.synchronize()
+        check_accept(p, q, x, u, q_indptr, acc.cpu().numpy(), tok.cpu().numpy())
+    with pytest.raises(nsd.NsdError):
+        nsd.spec_accept(t(p, torch.float32), t(q, torch.float32), t(x, torch.int32),
+                        t(u, torch.float32), t(q_indptr, torch.int32), mk, workspace=ws[:64])
+
+
 def test_first_token_follows_target_row(device):
     # speculative-sampling theorem on the GPU: 200k requests share (p_0, q_0)
     from scipy import stats
