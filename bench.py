@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--unfused", action="store_true",
                     help="kv_gather and verify_attention as separate kernels")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the practical-ceiling probe of the dominant kernel's access pattern")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy three times (counter calibration)")
     ap.add_argument("--h2d", action="store_true",
@@ -52,6 +54,10 @@ def parse():
     ap.add_argument("--schedule", action="store_true",
                     help="host-side scheduler (no GPU): batch-reconstruction decision latency "
                          "and a pool-scale simulation, the library against the oracle")
+    ap.add_argument("--sweep", action="store_true",
+                    help="every named round workload (tiny, draft_decode, verify_8b, knee, "
+                         "full_depth streamed layer by layer), one JSON line each, each with "
+                         "an oracle sample of --cpu-seconds")
     ap.add_argument("--draft-steps", type=int, default=4)
     ap.add_argument("--draft-vocab", type=int, default=151936)
     args = ap.parse_args()
@@ -124,6 +130,75 @@ def algorithmic_bytes(cfg, meta, acc_len=None):
     return {"gather": L * gather, "attention": L * attn, "fused": L * fused, "accept": accept}
 
 
+def practical_ceiling(dev, read_bytes, write_bytes, reps=7):
+    """What the memory system gives the attention pass's access pattern, measured
+    by a kernel that only moves the same bytes (libnsd_probe.so): 4 KiB tiles at
+    random positions, one persistent wave per SIMD with up to 32 KiB in flight,
+    and (for the fused pass) the written share of the tiles, at the end of every
+    wave's sequence, stored back to random positions right after they are read.  Returns the read-only rate and
+    the rate of the given read/write mix, in GB/s of bytes moved."""
+    import ctypes
+    import torch
+    from paper_2609_29364_amd.build import PROBE_LIB_PATH
+    lib = ctypes.CDLL(PROBE_LIB_PATH)
+    lib.nsd_probe_tiles.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                    ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    tile = 4096
+    waves = 4 * torch.cuda.get_device_properties(dev).multi_processor_count
+    steps = max(2, int(read_bytes / (waves * 4 * tile)))
+    n = waves * steps * 4
+    src_tiles = 2 * n
+    rng = np.random.default_rng(0)
+    src = torch.zeros(src_tiles * tile, dtype=torch.uint8, device=dev)
+    dst = torch.zeros(n * tile, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(waves * 1024, dtype=torch.uint8, device=dev)
+    ids = torch.as_tensor(rng.permutation(src_tiles)[:n].astype(np.int32), device=dev)
+    # the fused pass gives every wave its share of the arriving requests after its
+    # share of the resident ones: the written tiles are the last ones of every
+    # wave's sequence
+    frac = write_bytes / read_bytes if read_bytes else 0.0
+    step_in_wave = (np.arange(n) // 4) % steps
+    written = step_in_wave >= steps - int(round(frac * steps))
+    dids = np.where(written, rng.permutation(n), -1).astype(np.int32)
+    dids_d = torch.as_tensor(dids, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    sp = ctypes.c_void_p(stream.cuda_stream)
+
+    def run(with_writes):
+        st = lib.nsd_probe_tiles(src.data_ptr(), src_tiles, dst.data_ptr(), n, ids.data_ptr(),
+                                 dids_d.data_ptr() if with_writes else None, waves, steps,
+                                 sink.data_ptr(), sp)
+        if st != 0:
+            raise RuntimeError(f"nsd_probe_tiles status {st}")
+
+    out = {}
+    for key, wr in (("read_only_gbs", False), ("mix_gbs", True)):
+        if wr and not write_bytes:
+            out[key] = out["read_only_gbs"]
+            continue
+        run(wr)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record(stream)
+        for k in range(reps):
+            run(wr)
+            ev[k + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(reps)]))
+        moved = n * tile + (int(written.sum()) * tile if wr else 0)
+        out[key] = round(moved / (ms * 1e-3) / 1e9, 1)
+    out["write_share"] = round(float(written.mean()), 4)
+    out["pattern"] = (f"random 4 KiB tiles, {waves} persistent waves, up to 32 KiB in flight "
+                      f"per wave, {n * tile / 1e9:.2f} GB read"
+                      + (f", the last {written.mean():.1%} of every wave's tiles written back"
+                         if write_bytes else ""))
+    del src, dst, sink, ids, dids_d
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
     """The CPU oracle, untuned, on a bounded sample of the same round."""
     import oracle
@@ -136,7 +211,7 @@ def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
     rng = np.random.default_rng(0)
     order = rng.permutation(cfg.bs)
     p = acc_in.p_target if acc_in is not None else None
-    done, t_total = 0, 0.0
+    done, t_total, t_layer, t_acc = 0, 0.0, 0.0, 0.0
     u16 = lambda t: t.view(__import__("torch").int16).cpu().numpy()
     for r in order:
         # host copies of this request's inputs (not timed)
@@ -160,19 +235,26 @@ def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
         if meta.arriving[r]:
             oracle.gather.kv_gather(sk, sv, dk, dv, np.arange(nb), np.arange(nb))
         oracle.attention.verify_attention_request(q64, k64, v64, 1.0 / np.sqrt(cfg.head_dim))
+        t1 = time.perf_counter()
         if acc_in is not None:
             oracle.accept.accept_request(pr, qr, xr, ur)
-        t_total += time.perf_counter() - t0
+        t2 = time.perf_counter()
+        t_layer += t1 - t0
+        t_acc += t2 - t1
+        t_total += t2 - t0
         done += 1
         if t_total >= budget_s and done >= 2:
             break
-    layers = cfg.num_layers
-    per_req = t_total / done * layers if layers > 1 else t_total / done
+    # a round of several layers repeats the per-layer work (layer 0's sample
+    # stands for every layer) and accepts once
+    per_req = (t_layer * cfg.num_layers + t_acc) / done
     return {"value": round(1.0 / per_req, 3), "unit": "requests/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{done} of {cfg.bs} requests of the {cfg.name} round (gather of their "
                       f"blocks if arriving, attention over all heads/queries, acceptance), "
-                      f"{t_total:.1f} s of fp64 numpy"}
+                      f"{t_total:.1f} s of fp64 numpy"
+                      + (f"; layer 0 timed, counted for all {cfg.num_layers} layers"
+                         if cfg.num_layers > 1 else "")}
 
 
 def h2d_bench(args):
@@ -665,6 +747,92 @@ def draft_cpu_baseline(cfg, dd, budget_s):
                       f"fp64 numpy"}
 
 
+def sweep_bench(args):
+    """Every named round workload, one JSON line each (the default bench line is
+    verify_8b).  A step is the fused preparation + attention pass of every
+    layer, then acceptance.  The 36-layer round does not fit in HBM at once, so
+    it is streamed: each layer's inputs are generated (untimed), its pass is
+    timed with HIP events, and the round time is the sum over the layers plus
+    one acceptance."""
+    import torch
+    import paper_2609_29364_amd as nsd
+    from workload import CONFIGS, make_meta, make_layer, make_accept
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    i32 = lambda a: torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32, device=dev)
+
+    def timed(fn, warm, n):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev[0].record(stream)
+        for k in range(n):
+            fn()
+            ev[k + 1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(n)]))
+
+    for name in ("tiny", "draft_decode", "verify_8b", "knee", "full_depth"):
+        cfg = CONFIGS[name]
+        meta = make_meta(cfg)
+        bt, st, sl, qi = (i32(meta.block_table), i32(meta.stage_table), i32(meta.seq_lens),
+                          i32(meta.q_indptr))
+        ws = nsd.new_workspace(nsd.verify_attention_workspace_size(
+            cfg.bs, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, meta.max_q,
+            meta.max_seq_len), dev)
+        reps = max(3, args.steps // 5) if cfg.num_layers > 1 else args.steps
+        layer_ms = []
+        lay0 = None
+        for l in range(cfg.num_layers):
+            lay = make_layer(cfg, meta, l, dev)
+            out = torch.empty_like(lay.q)
+            layer_ms.append(timed(lambda: nsd.gather_verify_attention(
+                lay.q, lay.k_pool, lay.v_pool, lay.k_stage, lay.v_stage, bt, st, sl, qi,
+                meta.max_q, meta.max_seq_len, out=out, workspace=ws), args.warmup, reps))
+            if l == 0 and not args.no_cpu_baseline:
+                lay0 = lay          # the oracle sample uses layer 0's inputs
+            del lay, out
+            if cfg.num_layers > 1:
+                torch.cuda.empty_cache()
+        acc_in = make_accept(cfg, meta, dev)
+        acc_ms, acc_host = 0.0, None
+        if acc_in is not None:
+            al = torch.empty(cfg.bs, dtype=torch.int32, device=dev)
+            tk = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
+            aw = torch.empty(nsd.accept_workspace_size(cfg.bs, cfg.vocab), dtype=torch.uint8,
+                             device=dev)
+            acc_ms = timed(lambda: nsd.spec_accept(
+                acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens, acc_in.uniforms, qi,
+                int(meta.depth.max()), accepted_len=al, out_tokens=tk, workspace=aw),
+                args.warmup, args.steps)
+            acc_host = al.cpu().numpy()
+        alg = algorithmic_bytes(cfg, meta, acc_host)
+        fused_ms = float(np.sum(layer_ms))
+        round_ms = fused_ms + acc_ms
+        res = {"mode": "sweep", "workload": name, "config": describe(cfg),
+               "value": round(cfg.bs / (round_ms * 1e-3), 1), "unit": "requests/s",
+               "ms_per_round": round(round_ms, 4),
+               "fused_ms": round(fused_ms, 4), "accept_ms": round(acc_ms, 4),
+               "fused_layer_ms": [round(x, 4) for x in layer_ms] if cfg.num_layers > 1 else None,
+               "bytes": alg,
+               "fused_tbs": round(alg["fused"] / (fused_ms * 1e-3) / 1e12, 3),
+               "fused_frac": round(alg["fused"] / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+               "gather_attention_tbs": round((alg["gather"] + alg["attention"]) /
+                                             (fused_ms * 1e-3) / 1e12, 3),
+               "accept_tbs": (round(alg["accept"] / (acc_ms * 1e-3) / 1e12, 3)
+                              if acc_ms > 0 else None),
+               "timing": f"median of {reps} passes per layer after {args.warmup} warm-up, "
+                         f"HIP events on the launching stream"}
+        if lay0 is not None:
+            res["cpu_baseline"] = cpu_baseline(cfg, meta, lay0, acc_in, args.cpu_seconds)
+        print(json.dumps(res), flush=True)
+        del meta, lay0, acc_in, ws
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -684,6 +852,9 @@ def main():
         return
     if args.phi:
         phi_bench(args)
+        return
+    if args.sweep:
+        sweep_bench(args)
         return
     import torch
     import paper_2609_29364_amd as nsd
@@ -783,6 +954,15 @@ def main():
                      "alg_bytes_per_launch": kb},
         "wall_s_timed": round(t_wall, 3),
     }
+    if not args.no_ceiling:
+        # the dominant kernel's own read/write mix: the fused pass writes the staged
+        # blocks back; attention alone only reads
+        w = 0 if args.unfused else alg["gather"] // 2
+        ceil = practical_ceiling(dev, kb - w, w)
+        c = ceil["mix_gbs"]
+        result["roofline"]["practical"] = {"ceiling_gbs": c, "frac": round(achieved / c, 4),
+                                           "read_only_gbs": ceil["read_only_gbs"],
+                                           "pattern": ceil["pattern"]}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, meta, layer, acc_in, args.cpu_seconds)
     print(json.dumps(result), flush=True)

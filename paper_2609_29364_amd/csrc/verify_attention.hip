@@ -21,8 +21,8 @@
 //   contiguous per instruction), and P^T is exactly the S^T accumulator
 //   layout (converted to bf16), with no data exchange between lanes.  O^T
 //   accumulates per lane for one query row, so the online-softmax rescale is
-//   lane-local.  No LDS round trip is needed for either operand; Q operands
-//   sit in LDS in operand order.
+//   lane-local.  No LDS round trip is needed for either operand; an item's Q
+//   operands stay in registers.
 // * K/V are streamed once, so they are loaded non-temporally.  The registers
 //   loaded for one span are exactly the tile bytes, so the fused variant
 //   stores them back unchanged into the worker pool.
@@ -33,17 +33,21 @@
 // * Software pipeline: within an item K(j+1) is requested as soon as S(j)
 //   consumed K(j) and V(j+1) as soon as PV(j) consumed V(j); across items the
 //   next item's first span is requested during the current item's last span
-//   and its Q is fetched one item ahead, so a wave never drains its loads at
-//   an item boundary.  Block ids are wave-uniform scalar loads; every vector
+//   (and, where registers allow, its Q is fetched one item ahead), so a wave
+//   never drains its K/V loads at an item boundary.  Block ids are wave-uniform scalar loads; every vector
 //   load inside a loop is unconditional (a conditional load makes the
 //   compiler wait for all outstanding loads at the join).
 // * Load balance (stream-K): the spans of all (request, KV head) items are cut
 //   into as many equal contiguous ranges as the device keeps waves resident,
-//   whatever the spread of context lengths.  The split is static: the
-//   workspace needs no initialisation and no wave waits on another.  Items cut by a range boundary
-//   leave partials that a small second kernel merges in range order
-//   (deterministic, no atomics in the arithmetic); all other items are
-//   written directly.
+//   whatever the spread of context lengths.  The fused variant cuts the
+//   resident and the arriving requests' spans separately and every wave takes
+//   one range of each, resident first, so that all waves write the staged
+//   tiles in the same phase of the launch (writes gathered in time cost HBM
+//   less than writes spread through the read stream).  The split is static:
+//   the workspace needs no initialisation and no wave waits on another.
+//   Items cut by a range boundary leave partials that a small second kernel
+//   merges in range order (deterministic, no atomics in the arithmetic); all
+//   other items are written directly.
 // * Masked tokens (past a query's position, past L_r, or in a block whose id
 //   is out of range) are removed by selection: scores become -inf and V
 //   elements past L_r are zeroed, so NaN-filled unused slots never leak.
@@ -83,9 +87,10 @@ struct Params {
   const int32_t* seq_lens;
   const int32_t* q_indptr;
   uint16_t* out;
-  float* part_o;       // [2 * ranges][MT*16][D]: head/tail partial O per range
-  float2* part_ml;     // [2 * ranges][MT*16]: (running max, sum)
-  uint32_t* prefix;    // [bs+1]: exclusive prefix of per-request span counts
+  float* part_o;       // [4 * waves][MT*16][D]: head/tail partial O per range
+  float2* part_ml;     // [4 * waves][MT*16]: (running max, sum)
+  uint32_t* prefix;    // [bs+1]: exclusive span prefix over the work order's positions
+  uint32_t* pos_of;    // [bs+1]: position of each request; [bs]: resident requests
   int32_t num_blocks;    // blocks in the worker pool (tiles fit 32-bit indexes)
   int32_t stage_blocks;  // blocks in the staging pool (0 without fusion)
   int32_t bs;
@@ -96,7 +101,8 @@ struct Params {
   int32_t max_q;
   int32_t max_seq_len;
   int32_t num_waves;
-  int32_t w_even, w_odd;   // relative range lengths of waves on even / odd XCDs
+  int32_t w_even;          // relative range length of waves on even XCDs
+  int32_t w_odd, w_odd_b;  // ... on odd XCDs, resident / arriving segment
   float scale_log2;  // softmax scale * log2(e)
 };
 
@@ -177,51 +183,49 @@ __device__ inline int spans_of(int L) {
   return max(1, (L + NB * kBlock - 1) / (NB * kBlock));
 }
 
-// Work units of one span in the stream-K split.  In the fused variant a span
-// of an arriving request also writes its tiles to the worker pool, which costs
-// HBM time beside the read; the split weighs it accordingly.
-constexpr int kResidentCost = 4;
-constexpr int kArrivingCost = 6;
-
 __device__ inline bool is_arriving(const Params& p, const int32_t* __restrict__ stage_table,
                                    int r) {
   return p.stage_blocks > 0 && stage_table[(int64_t)r * p.max_blocks_per_seq] >= 0;
 }
 
-__device__ inline int ceil_div_pos(int64_t a, int c) { return a <= 0 ? 0 : (int)((a + c - 1) / c); }
+// Spans of an item (n spans from span position base) that lie in [b, e).
+__device__ inline void spans_in(int64_t base, int n, int64_t b, int64_t e, int& j0, int& j1) {
+  j0 = (int)max((int64_t)0, min((int64_t)n, b - base));
+  j1 = (int)max((int64_t)0, min((int64_t)n, e - base));
+}
 
-// Spans of an item (n spans of c units from unit position base) whose start
-// lies in [b, e).
-__device__ inline void spans_in(int64_t base, int c, int n, int64_t b, int64_t e, int& j0,
-                                int& j1) {
-  j0 = min(n, ceil_div_pos(b - base, c));
-  j1 = min(n, ceil_div_pos(e - base, c));
+// Request at position i of the work order: the fused variant orders the
+// batch resident requests first, then arriving ones; otherwise position i is
+// request i.
+template <bool FUSE>
+__device__ inline int request_at(const uint16_t* order, int i) {
+  return FUSE ? (int)order[i] : i;
 }
 
 // One (request r, KV head g) item restricted to the spans [j0, j1) whose
 // start lies in a range.
 struct Item {
-  int r, g, L, n, c, qo, nq, rows, win, j0, j1;
-  int64_t pr;        // exclusive unit prefix of request r (per KV head)
-  int64_t base;      // unit position of the item's first span
+  int pos, r, g, L, n, qo, nq, rows, win, j0, j1;
+  int64_t pr;        // exclusive span prefix of position pos (per KV head)
+  int64_t base;      // span position of the item's first span
   bool arriving;     // fused variant: K/V come from the staging pool
 };
 
 template <int NB, bool FUSE>
 __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
-                                 const int32_t* __restrict__ stage_table, int r, int g,
-                                 int64_t pr, int64_t s, int64_t s1) {
+                                 const int32_t* __restrict__ stage_table, int pos, int r,
+                                 int g, int64_t pr, int64_t s, int64_t s1) {
   Item it;
+  it.pos = pos;
   it.r = r;
   it.g = g;
   it.pr = pr;
   it.L = clamp_len(p, seq_lens, r);
   it.n = spans_of<NB>(it.L);
   it.arriving = FUSE && is_arriving(p, stage_table, r);
-  it.c = it.arriving ? kArrivingCost : kResidentCost;
-  it.base = (int64_t)p.num_kv_heads * pr + (int64_t)g * it.n * it.c;
-  spans_in(it.base, it.c, it.n, s, s1, it.j0, it.j1);
+  it.base = (int64_t)p.num_kv_heads * pr + (int64_t)g * it.n;
+  spans_in(it.base, it.n, s, s1, it.j0, it.j1);
   it.qo = q_indptr[r];
   it.nq = max(0, min(q_indptr[r + 1] - it.qo, p.max_q));
   it.rows = p.group * it.nq;
@@ -229,16 +233,18 @@ __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ se
   return it;
 }
 
-// The item after `it` in (request, KV head) order.
+// The item after `it` in (position, KV head) order; `it` is not the last
+// item of the order.
 template <int NB, bool FUSE>
 __device__ inline Item next_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
-                                 const int32_t* __restrict__ stage_table, const Item& it,
-                                 int64_t s, int64_t s1) {
+                                 const int32_t* __restrict__ stage_table, const uint16_t* order,
+                                 const Item& it, int64_t s, int64_t s1) {
   const bool nr = it.g == p.num_kv_heads - 1;
-  return make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, nr ? it.r + 1 : it.r,
-                             nr ? 0 : it.g + 1, nr ? it.pr + (int64_t)it.n * it.c : it.pr, s,
-                             s1);
+  const int pos = nr ? it.pos + 1 : it.pos;
+  return make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos,
+                             nr ? uniform(request_at<FUSE>(order, pos)) : it.r, nr ? 0 : it.g + 1,
+                             nr ? it.pr + it.n : it.pr, s, s1);
 }
 
 // Raw block-table entries of one span (scalar loads, checked later).
@@ -605,9 +611,9 @@ __device__ inline void finish_item(const Params& p, Acc<D, MT>& a, const Item& i
   }
 }
 
-// The global sequence of T work units (spans in request, KV head, position
-// order, each span weighing its unit cost) is cut into W contiguous ranges,
-// one per resident wave, sized by the wave's speed: workgroups are dealt to
+// A segment's sequence of T spans (in work-order position, KV head, span
+// order) is cut into W contiguous ranges, one per resident wave, sized by the
+// wave's speed: workgroups are dealt to
 // the eight XCDs in turn, and waves on odd XCDs stream HBM measurably slower
 // than those on even ones, so their ranges are shorter in the ratio
 // w_odd : w_even.  Every kernel derives the same ranges from T, W and the
@@ -625,7 +631,7 @@ struct Ranges {
   }
   __device__ int64_t begin(int64_t rid) const { return T * weight_before(rid) / total; }
   __device__ int64_t end(int64_t rid) const { return T * weight_before(rid + 1) / total; }
-  // range holding unit s: the last q with begin(q) <= s, i.e. the last q
+  // range holding span s: the last q with begin(q) <= s, i.e. the last q
   // with weight_before(q) <= G = floor(((s + 1) * total - 1) / T), found by
   // inverting the piecewise-linear weight_before
   __device__ int64_t of(int64_t s) const {
@@ -638,8 +644,8 @@ struct Ranges {
   }
 };
 
-// Request whose spans [hkv*pre[r], hkv*pre[r+1]) contain global span s.
-__device__ inline int find_request(const uint32_t* pre, int bs, int hkv, int64_t s) {
+// Work-order position whose spans [hkv*pre[i], hkv*pre[i+1]) contain span s.
+__device__ inline int find_position(const uint32_t* pre, int bs, int hkv, int64_t s) {
   int lo = 0, hi = bs - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -688,34 +694,35 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
                               const int32_t* __restrict__ stage_table,
                               const int32_t* __restrict__ seq_lens,
                               const int32_t* __restrict__ q_indptr, const uint32_t* pre,
-                              int total_q, int64_t rid, int64_t s,
+                              const uint16_t* order, int total_q, int64_t rid, int64_t s,
                               int64_t s1, int lane) {
   const int hkv = p.num_kv_heads;
-  const int r0 = uniform(find_request(pre, p.bs, hkv, s));
-  const int64_t pr0 = uniform64(pre[r0]);
-  // the item holding unit position s; it is empty here when s falls inside
-  // its last span (that span belongs to the range where it starts)
-  const int nc0 = spans_of<NB>(clamp_len(p, seq_lens, r0)) *
-                  (FUSE && is_arriving(p, stage_table, r0) ? kArrivingCost : kResidentCost);
-  const int g0 = (int)min((int64_t)hkv - 1, (s - (int64_t)hkv * pr0) / nc0);
-  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, r0, g0, pr0, s, s1);
+  const int pos0 = uniform(find_position(pre, p.bs, hkv, s));
+  const int r0 = uniform(request_at<FUSE>(order, pos0));
+  const int64_t pr0 = uniform64(pre[pos0]);
+  // the item holding span position s
+  const int n0 = spans_of<NB>(clamp_len(p, seq_lens, r0));
+  const int g0 = (int)min((int64_t)hkv - 1, (s - (int64_t)hkv * pr0) / n0);
+  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos0, r0, g0, pr0, s, s1);
   if (it.j0 >= it.j1) {
-    if (it.r == p.bs - 1 && it.g == hkv - 1) return;
-    it = next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, it, s, s1);
-    if (it.j0 >= it.j1) return;   // no span starts in this range
+    if (it.pos == p.bs - 1 && it.g == hkv - 1) return;
+    it = next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, it, s, s1);
+    if (it.j0 >= it.j1) return;   // no span lies in this range
   }
-  // next item with a span starting in the range (or `it` itself when none)
+  // next item with a span in the range (or `it` itself when none)
   auto following = [&](const Item& cur) {
-    const bool last = cur.r == p.bs - 1 && cur.g == hkv - 1;
-    if (last || cur.base + (int64_t)cur.n * cur.c >= s1) return cur;
-    return next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, cur, s, s1);
+    const bool last = cur.pos == p.bs - 1 && cur.g == hkv - 1;
+    if (last || cur.base + (int64_t)cur.n >= s1) return cur;
+    return next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, cur, s, s1);
   };
   Item next = following(it);
   bool more = next.base != it.base;
 
   // Q of the next item is fetched one item ahead when the tile leaves room
-  // for a second copy (PREQ); larger tiles fetch it at the switch.
-  constexpr bool PREQ = D * MT <= 256;
+  // for a second copy (PREQ); larger tiles, and the fused variant (whose
+  // store path needs the registers: a second copy spilled to scratch memory
+  // and cost 5 % of the pass), fetch it at the switch.
+  constexpr bool PREQ = D * MT <= 256 && !FUSE;
   QOps<MT, D> qc, qn;
   load_q<D, MT>(qc, p, it, total_q, lane);
   SpanRef<NB> cur =
@@ -748,8 +755,27 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
   }
 }
 
-// One dispatch of W waves (W / 4 workgroups of 4 independent waves), one
-// range each.
+// Sum of x over the workgroup's 256 threads, in every thread.
+__device__ inline uint32_t block_sum(uint32_t x, uint32_t* s_tmp, int lane, int wave) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  __syncthreads();   // s_tmp may still be read from the previous call
+  if (lane == 0) s_tmp[wave] = x;
+  __syncthreads();
+  return s_tmp[0] + s_tmp[1] + s_tmp[2] + s_tmp[3];
+}
+
+// One dispatch of W waves (W / 4 workgroups of 4 independent waves).
+//
+// Work order: the fused variant places the batch's resident requests first
+// (positions [0, nA)) and its arriving requests after them, each group in
+// request order; the spans of the two segments are split separately into W
+// ranges each, and wave w takes range w of both segments, one after the
+// other.  Every wave therefore does its share of the arriving requests (the
+// reads and the write-back of staged tiles) in the same phase of the launch:
+// HBM serves reads and writes gathered in time markedly faster than the same
+// writes spread through a read stream.  Without fusion there is one segment
+// and position i is request i.
 template <int D, int MT, bool FUSE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
 void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
@@ -757,52 +783,97 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
                              const int32_t* __restrict__ seq_lens,
                              const int32_t* __restrict__ q_indptr) {
   constexpr int NB = span_blocks(D, MT);
-  extern __shared__ uint32_t s_pre[];        // [bs + 1]: exclusive prefix of per-request spans
-  __shared__ uint32_t s_wsum[4];
+  extern __shared__ uint32_t s_pre[];   // [bs + 1] span prefix by position, then uint16 order[bs]
+  uint16_t* s_order = (uint16_t*)(s_pre + p.bs + 1);
+  __shared__ uint32_t s_wsum[3][4];
+  __shared__ uint32_t s_red[4];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = uniform(tid >> 6);
   const int total_q = uniform(q_indptr[p.bs]);
 
-  // prefix of per-request work units (spans times their unit cost); every
-  // workgroup keeps its own copy
-  uint32_t carry = 0;
+  // resident requests and their spans (the first segment)
+  uint32_t n_res = p.bs, u_res = 0;
+  if constexpr (FUSE) {
+    uint32_t c = 0, u = 0;
+    for (int r = tid; r < p.bs; r += 256)
+      if (!is_arriving(p, stage_table, r)) {
+        ++c;
+        u += spans_of<NB>(clamp_len(p, seq_lens, r));
+      }
+    n_res = block_sum(c, s_red, lane, wave);
+    u_res = block_sum(u, s_red, lane, wave);
+  }
+  // positions and span prefixes; every workgroup keeps its own copy, the
+  // first also stores them for the merge kernel
+  uint32_t c_arr = 0, c_ua = 0, c_ur = 0;   // before the chunk: arriving requests,
+                                            // their spans, resident spans
   for (int base = 0; base < p.bs; base += 256) {
     const int r = base + tid;
-    const uint32_t n =
-        r < p.bs ? spans_of<NB>(clamp_len(p, seq_lens, r)) *
-                       (FUSE && is_arriving(p, stage_table, r) ? kArrivingCost : kResidentCost)
-                 : 0;
-    uint32_t incl = n;
+    const bool in = r < p.bs;
+    const bool arr = in && FUSE && is_arriving(p, stage_table, r);
+    const uint32_t n = in ? spans_of<NB>(clamp_len(p, seq_lens, r)) : 0;
+    uint32_t v[3] = {arr ? 1u : 0u, arr ? n : 0u, arr ? 0u : n};
+    uint32_t incl[3] = {v[0], v[1], v[2]};
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t y = __shfl_up(incl, o);
-      if (lane >= o) incl += y;
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        const uint32_t y = __shfl_up(incl[k], o);
+        if (lane >= o) incl[k] += y;
+      }
     }
-    if (lane == 63) s_wsum[wave] = incl;
+    if (lane == 63) {
+#pragma unroll
+      for (int k = 0; k < 3; ++k) s_wsum[k][wave] = incl[k];
+    }
     __syncthreads();
-    uint32_t before = carry;
-    for (int i = 0; i < wave; ++i) before += s_wsum[i];
-    if (r < p.bs) {
-      s_pre[r] = before + incl - n;
-      if (blockIdx.x == 0) p.prefix[r] = before + incl - n;
+    uint32_t before[3] = {c_arr, c_ua, c_ur};
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+      for (int i = 0; i < wave; ++i) before[k] += s_wsum[k][i];
+    if (in) {
+      const uint32_t a_before = before[0] + incl[0] - v[0];
+      const int pos = arr ? (int)(n_res + a_before) : r - (int)a_before;
+      const uint32_t pre = arr ? u_res + before[1] + incl[1] - v[1] : before[2] + incl[2] - v[2];
+      s_pre[pos] = pre;
+      if constexpr (FUSE) s_order[pos] = (uint16_t)r;
+      if (blockIdx.x == 0) {
+        p.prefix[pos] = pre;
+        p.pos_of[r] = pos;
+      }
     }
-    carry += s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
+    c_arr += s_wsum[0][0] + s_wsum[0][1] + s_wsum[0][2] + s_wsum[0][3];
+    c_ua += s_wsum[1][0] + s_wsum[1][1] + s_wsum[1][2] + s_wsum[1][3];
+    c_ur += s_wsum[2][0] + s_wsum[2][1] + s_wsum[2][2] + s_wsum[2][3];
     __syncthreads();
   }
   if (tid == 0) {
-    s_pre[p.bs] = carry;
-    if (blockIdx.x == 0) p.prefix[p.bs] = carry;
+    s_pre[p.bs] = c_ua + c_ur;
+    if (blockIdx.x == 0) {
+      p.prefix[p.bs] = c_ua + c_ur;
+      p.pos_of[p.bs] = n_res;
+    }
   }
   __syncthreads();
   if (total_q <= 0) return;   // no query rows: nothing to attend
 
-  const Ranges R((int64_t)p.num_kv_heads * carry, p.num_waves, p.w_even, p.w_odd);
+  const int64_t hkv = p.num_kv_heads;
+  const int64_t ta = hkv * s_pre[n_res], tb = hkv * s_pre[p.bs] - ta;
+  const Ranges ra(ta, p.num_waves, p.w_even, p.w_odd), rb(tb, p.num_waves, p.w_even, p.w_odd_b);
   const int64_t rid = (int64_t)blockIdx.x * 4 + wave;
-  const int64_t b = uniform64(R.begin(rid)), e = uniform64(R.end(rid));
-  if (b < e)
-    process_range<D, MT, NB, FUSE>(p, block_table, stage_table, seq_lens, q_indptr, s_pre,
-                                   total_q, rid, b, e, lane);
+  // resident range first, then the arriving range (writes last)
+#pragma unroll 1
+  for (int k = 0; k < (FUSE ? 2 : 1); ++k) {
+    const bool seg_b = k == 1;
+    const Ranges& R = seg_b ? rb : ra;
+    const int64_t off = seg_b ? ta : 0;
+    const int64_t b = uniform64(off + R.begin(rid)), e = uniform64(off + R.end(rid));
+    if (b < e)
+      process_range<D, MT, NB, FUSE>(p, block_table, stage_table, seq_lens, q_indptr, s_pre,
+                                     s_order, total_q, seg_b ? p.num_waves + rid : rid, b, e,
+                                     lane);
+  }
 }
 
 // Merge the partials of every item that a range boundary cut, in range order
@@ -818,15 +889,22 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const int r = blockIdx.y;
   const int hkv = p.num_kv_heads;
   const int tid = threadIdx.x;
-  const Ranges R((int64_t)hkv * p.prefix[p.bs], p.num_waves, p.w_even, p.w_odd);
+  // the segment holding request r's position, and its ranges
+  const int n_res = (int)p.pos_of[p.bs];
+  const int pos = (int)p.pos_of[r];
+  const int64_t ta = (int64_t)hkv * p.prefix[n_res];
+  const bool seg_b = pos >= n_res;
+  const int64_t off = seg_b ? ta : 0;
+  const int64_t qoff = seg_b ? p.num_waves : 0;
+  const Ranges R(seg_b ? (int64_t)hkv * p.prefix[p.bs] - ta : ta, p.num_waves, p.w_even,
+                 seg_b ? p.w_odd_b : p.w_odd);
   const int L = clamp_len(p, p.seq_lens, r);
   const int n = spans_of<NB>(L);
-  const int c = is_arriving(p, p.stage_table, r) ? kArrivingCost : kResidentCost;
   const int qo = p.q_indptr[r];
   const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
-  const int64_t base = (int64_t)p.prefix[r] * hkv + (int64_t)g * n * c;
-  const int64_t ra = uniform64(R.of(base));                          // first span's range
-  const int64_t rb = uniform64(R.of(base + (int64_t)(n - 1) * c));   // last span's range
+  const int64_t base = (int64_t)p.prefix[pos] * hkv + (int64_t)g * n;
+  const int64_t ra = uniform64(R.of(base - off));           // first span's range
+  const int64_t rb = uniform64(R.of(base - off + n - 1));   // last span's range
   if (ra == rb || nq == 0) return;
   const int rows = p.group * nq;
   constexpr int kVec = D / 4;
@@ -845,8 +923,8 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
     const int64_t q = q0 + tid;
     if (q <= rb) {
       int j0, j1;
-      spans_in(base, c, n, R.begin(q), R.end(q), j0, j1);
-      s_slot[tid] = j0 < j1 ? 2 * q + (j0 > 0 ? 0 : 1) : -1;
+      spans_in(base, n, off + R.begin(q), off + R.end(q), j0, j1);
+      s_slot[tid] = j0 < j1 ? 2 * (qoff + q) + (j0 > 0 ? 0 : 1) : -1;
     }
     __syncthreads();
     if (tid == 0) {   // keep the ranges holding a part, in order
@@ -964,9 +1042,10 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool 
   if (rows > kMaxRows) return false;
   pl->mt = (rows + 15) / 16;
   pl->num_waves = resident_waves(d, pl->mt, fuse);
-  const size_t slots = 2 * (size_t)pl->num_waves * pl->mt * 16;
-  pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t);
-  pl->prefix_bytes = (((size_t)bs + 1) * sizeof(uint32_t) + 255) / 256 * 256;
+  // a head and a tail slot per range, W ranges in each of the two segments
+  const size_t slots = 4 * (size_t)pl->num_waves * pl->mt * 16;
+  pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t) + ((size_t)bs * sizeof(uint16_t) + 3) / 4 * 4;
+  pl->prefix_bytes = (2 * ((size_t)bs + 1) * sizeof(uint32_t) + 255) / 256 * 256;
   pl->part_o_bytes = slots * d * sizeof(float);
   pl->part_ml_bytes = slots * sizeof(float2);
   pl->ws_bytes = pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes;
@@ -974,20 +1053,20 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool 
 }
 
 template <int D, int MT, bool FUSE>
-void launch(const Params& p, int bs, hipStream_t stream) {
+void launch(const Params& p, int bs, size_t lds_bytes, hipStream_t stream) {
   hipLaunchKernelGGL((verify_attention_kernel<D, MT, FUSE>), dim3(p.num_waves / 4), dim3(256),
-                     ((size_t)bs + 1) * sizeof(uint32_t), stream, p, p.block_table,
-                     p.stage_table, p.seq_lens, p.q_indptr);
+                     lds_bytes, stream, p, p.block_table, p.stage_table, p.seq_lens,
+                     p.q_indptr);
   hipLaunchKernelGGL((combine_kernel<D, MT>), dim3(p.num_kv_heads, bs), dim3(256), 0, stream, p);
 }
 
 template <int D, bool FUSE>
-void launch_d(const Params& p, int mt, int bs, hipStream_t stream) {
+void launch_d(const Params& p, int mt, int bs, size_t lds_bytes, hipStream_t stream) {
   switch (mt) {
-    case 1: launch<D, 1, FUSE>(p, bs, stream); break;
-    case 2: launch<D, 2, FUSE>(p, bs, stream); break;
-    case 3: launch<D, 3, FUSE>(p, bs, stream); break;
-    default: launch<D, 4, FUSE>(p, bs, stream); break;
+    case 1: launch<D, 1, FUSE>(p, bs, lds_bytes, stream); break;
+    case 2: launch<D, 2, FUSE>(p, bs, lds_bytes, stream); break;
+    case 3: launch<D, 3, FUSE>(p, bs, lds_bytes, stream); break;
+    default: launch<D, 4, FUSE>(p, bs, lds_bytes, stream); break;
   }
 }
 
@@ -1058,6 +1137,7 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   p.out = (uint16_t*)out;
   char* ws = (char*)workspace;
   p.prefix = (uint32_t*)ws;
+  p.pos_of = p.prefix + bs + 1;
   p.part_o = (float*)(ws + pl.prefix_bytes);
   p.part_ml = (float2*)(ws + pl.prefix_bytes + pl.part_o_bytes);
   p.num_blocks = (int32_t)num_blocks;
@@ -1070,19 +1150,21 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   p.max_q = max_q_per_seq;
   p.max_seq_len = max_seq_len;
   p.num_waves = pl.num_waves;
-  // measured HBM streaming speed of odd-XCD waves relative to even ones (the
-  // fused pass also writes, which widens the gap)
+  // measured HBM streaming speed of odd-XCD waves relative to even ones, in
+  // the read-only resident segment and in the arriving segment (which also
+  // writes, widening the gap)
   p.w_even = 100;
-  p.w_odd = fuse ? 91 : 94;
+  p.w_odd = 94;
+  p.w_odd_b = 91;
   p.scale_log2 = scale * 1.4426950408889634f;
 
   clear_stale_error();
   if (fuse) {
-    if (head_dim == 64) launch_d<64, true>(p, pl.mt, bs, (hipStream_t)stream);
-    else launch_d<128, true>(p, pl.mt, bs, (hipStream_t)stream);
+    if (head_dim == 64) launch_d<64, true>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
+    else launch_d<128, true>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
   } else {
-    if (head_dim == 64) launch_d<64, false>(p, pl.mt, bs, (hipStream_t)stream);
-    else launch_d<128, false>(p, pl.mt, bs, (hipStream_t)stream);
+    if (head_dim == 64) launch_d<64, false>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
+    else launch_d<128, false>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
   }
   return check_launch(fn);
 }

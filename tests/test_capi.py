@@ -144,3 +144,28 @@ def test_append_commit_alias_validation(lib):
     assert g(fake, None, fake, fake, 3, None) == 1
     out = ctypes.c_void_p()
     assert lib.nsd_host_alias(None, ctypes.byref(out)) == 1
+
+
+def test_probe_library_exports_and_validates():
+    """The bandwidth-probe library (measurement only) exports what its header
+    declares and refuses bad arguments before any launch."""
+    from paper_2609_29364_amd.build import PROBE_LIB_PATH, build
+    if not os.path.exists(PROBE_LIB_PATH):
+        build()
+    plib = ctypes.CDLL(PROBE_LIB_PATH)
+    src = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "nsd_probe.h")).read(),
+                 flags=re.S)
+    names = sorted(set(re.findall(r"\b(nsd_\w+)\s*\(", src)))
+    assert names == ["nsd_probe_tiles"]
+    for name in names:
+        assert hasattr(plib, name), name
+    f = plib.nsd_probe_tiles
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.c_void_p, ctypes.c_void_p]
+    fake = 16   # never dereferenced: every case fails before any launch
+    assert f(None, 8, None, 0, fake, None, 4, 1, fake, None) == 1        # no source
+    assert f(fake, 8, None, 8, fake, fake, 4, 1, fake, None) == 1        # writes without dst
+    assert f(fake, 8, None, 0, fake, None, 6, 1, fake, None) == 2        # waves % 4
+    assert f(fake, 0, None, 0, fake, None, 4, 1, fake, None) == 2        # empty source
+    assert f(fake, 8, None, 0, fake, None, 4, -1, fake, None) == 2       # steps < 0

@@ -99,6 +99,29 @@ def test_attention_edge_cases(device, case, waves, fused):
     _check_all(cfg, meta, device, waves=waves, fused=fused)
 
 
+ARRIVING_SETS = {
+    "none": [], "all": list(range(8)), "first": [0], "last": [7],
+    "head_half": [0, 1, 2, 3], "tail_half": [4, 5, 6, 7], "scattered": [1, 2, 6],
+}
+
+
+@pytest.mark.parametrize("waves", [None, 4, 12])
+@pytest.mark.parametrize("aset", sorted(ARRIVING_SETS))
+def test_fused_arriving_sets(device, aset, waves):
+    """The fused pass works on resident requests and arriving requests as two
+    segments, each split over the waves on its own; every arriving set (none,
+    all, one at either end, contiguous halves, scattered) gives the gather's
+    bytes and the oracle's attention."""
+    lens = [40, 300, 17, 129, 1, 64, 500, 33]
+    depth = [3, 4, 0, 8, 0, 2, 5, 1]
+    arriving = np.zeros(8, dtype=bool)
+    arriving[ARRIVING_SETS[aset]] = True
+    cfg = custom_config(seed=300, bs=8, num_q_heads=8, num_kv_heads=2, head_dim=128, vocab=0,
+                        n_arriving=int(arriving.sum()), pool_blocks=None)
+    meta = make_meta(cfg, seq_lens=lens, depth=depth, arriving=arriving)
+    _check_all(cfg, meta, device, waves=waves, fused=True)
+
+
 def test_ragged_batch_of_64(device):
     rng = np.random.default_rng(5)
     lens = rng.integers(1, 700, 64)
