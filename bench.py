@@ -36,6 +36,10 @@ def parse():
     ap.add_argument("--unfused", action="store_true",
                     help="kv_gather and verify_attention as separate kernels")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--ceiling", action="store_true",
+                    help="only the HBM probe: the fused pass's read/write mix on verify_8b with "
+                         "the written tiles placed three ways (gathered at the end of every "
+                         "wave's sequence, spread through it, or on a share of the waves)")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the practical-ceiling probe of the dominant kernel's access pattern")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -130,13 +134,18 @@ def algorithmic_bytes(cfg, meta, acc_len=None):
     return {"gather": L * gather, "attention": L * attn, "fused": L * fused, "accept": accept}
 
 
-def practical_ceiling(dev, read_bytes, write_bytes, reps=7):
+def practical_ceiling(dev, read_bytes, write_bytes, reps=7, placement="end"):
     """What the memory system gives the attention pass's access pattern, measured
     by a kernel that only moves the same bytes (libnsd_probe.so): 4 KiB tiles at
     random positions, one persistent wave per SIMD with up to 32 KiB in flight,
-    and (for the fused pass) the written share of the tiles, at the end of every
-    wave's sequence, stored back to random positions right after they are read.  Returns the read-only rate and
-    the rate of the given read/write mix, in GB/s of bytes moved."""
+    and (for the fused pass) the written share of the tiles stored back to
+    random positions right after they are read.  Returns the read-only rate and
+    the rate of the given read/write mix, in GB/s of bytes moved.
+
+    placement of the written tiles (same bytes): "end" the last share of every
+    wave's sequence (the fused pass's order); "spread" runs of 40 steps (one
+    request's item) scattered through every wave's sequence; "waves" every tile
+    of a share of the waves, the others only reading."""
     import ctypes
     import torch
     from paper_2609_29364_amd.build import PROBE_LIB_PATH
@@ -160,7 +169,14 @@ def practical_ceiling(dev, read_bytes, write_bytes, reps=7):
     # wave's sequence
     frac = write_bytes / read_bytes if read_bytes else 0.0
     step_in_wave = (np.arange(n) // 4) % steps
-    written = step_in_wave >= steps - int(round(frac * steps))
+    if placement == "end":
+        written = step_in_wave >= steps - int(round(frac * steps))
+    elif placement == "spread":
+        written = ((np.arange(n) // 4 // 40) * 7919 % 1000) < frac * 1000
+    elif placement == "waves":
+        written = ((np.arange(n) // (4 * steps)) * 7919 % 1000) < frac * 1000
+    else:
+        raise ValueError(placement)
     dids = np.where(written, rng.permutation(n), -1).astype(np.int32)
     dids_d = torch.as_tensor(dids, device=dev)
     stream = torch.cuda.current_stream(dev)
@@ -190,10 +206,13 @@ def practical_ceiling(dev, read_bytes, write_bytes, reps=7):
         moved = n * tile + (int(written.sum()) * tile if wr else 0)
         out[key] = round(moved / (ms * 1e-3) / 1e9, 1)
     out["write_share"] = round(float(written.mean()), 4)
+    where = {"end": f"the last {written.mean():.1%} of every wave's tiles",
+             "spread": f"{written.mean():.1%} of the tiles, in runs of 40 steps through every "
+                       f"wave's sequence",
+             "waves": f"every tile of {written.mean():.1%} of the waves"}[placement]
     out["pattern"] = (f"random 4 KiB tiles, {waves} persistent waves, up to 32 KiB in flight "
                       f"per wave, {n * tile / 1e9:.2f} GB read"
-                      + (f", the last {written.mean():.1%} of every wave's tiles written back"
-                         if write_bytes else ""))
+                      + (f", {where} written back" if write_bytes else ""))
     del src, dst, sink, ids, dids_d
     torch.cuda.empty_cache()
     return out
@@ -747,6 +766,25 @@ def draft_cpu_baseline(cfg, dd, budget_s):
                       f"fp64 numpy"}
 
 
+def ceiling_bench(args):
+    """The probe alone on the fused pass's bytes for the workload: one JSON line
+    with the read-only rate and the read + write-back rate for each placement
+    of the written tiles."""
+    import torch
+    from workload import CONFIGS, make_meta
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.workload]
+    meta = make_meta(cfg)
+    alg = algorithmic_bytes(cfg, meta)
+    w = alg["gather"] // 2
+    res = {"mode": "ceiling", "workload": cfg.name, "read_bytes": alg["fused"] - w,
+           "write_bytes": w}
+    for placement in ("end", "spread", "waves"):
+        res[placement] = practical_ceiling(dev, alg["fused"] - w, w, placement=placement)
+    print(json.dumps(res), flush=True)
+
+
 def sweep_bench(args):
     """Every named round workload, one JSON line each (the default bench line is
     verify_8b).  A step is the fused preparation + attention pass of every
@@ -855,6 +893,9 @@ def main():
         return
     if args.sweep:
         sweep_bench(args)
+        return
+    if args.ceiling:
+        ceiling_bench(args)
         return
     import torch
     import paper_2609_29364_amd as nsd
