@@ -805,13 +805,13 @@ def sweep_bench(args):
         for _ in range(warm):
             fn()
         torch.cuda.synchronize()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-        ev[0].record(stream)
-        for k in range(n):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
             fn()
-            ev[k + 1].record(stream)
+        b.record(stream)
         torch.cuda.synchronize()
-        return float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(n)]))
+        return a.elapsed_time(b) / n
 
     for name in ("tiny", "draft_decode", "verify_8b", "knee", "full_depth"):
         cfg = CONFIGS[name]
@@ -862,8 +862,8 @@ def sweep_bench(args):
                                              (fused_ms * 1e-3) / 1e12, 3),
                "accept_tbs": (round(alg["accept"] / (acc_ms * 1e-3) / 1e12, 3)
                               if acc_ms > 0 else None),
-               "timing": f"median of {reps} passes per layer after {args.warmup} warm-up, "
-                         f"HIP events on the launching stream"}
+               "timing": f"mean of {reps} back-to-back passes per layer after {args.warmup} "
+                         f"warm-up, HIP events on the launching stream"}
         if lay0 is not None:
             res["cpu_baseline"] = cpu_baseline(cfg, meta, lay0, acc_in, args.cpu_seconds)
         print(json.dumps(res), flush=True)
@@ -949,18 +949,24 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # the timed region: K whole steps back to back, nothing else on the stream
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
     for i in range(args.steps):
-        step(evs[i])
+        step()
     end.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
+    # per-kernel breakdown from the same steps run again with events between the
+    # kernels (an event record adds a few microseconds, so it stays out of the
+    # timed region)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
     parts = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
                       for e in evs])
     g_ms, a_ms, c_ms = parts.mean(0)

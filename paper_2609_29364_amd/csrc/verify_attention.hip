@@ -908,9 +908,10 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   if (ra == rb || nq == 0) return;
   const int rows = p.group * nq;
   constexpr int kVec = D / 4;
+  const int nel = rows * kVec;   // float4 elements of the item's rows
   // running merge over the ranges, 256 at a time (an item rarely spans more
   // than a few)
-  constexpr int kPer = (kMaxRows * kVec + 255) / 256;   // elements per thread
+  constexpr int kPer = (MT * 16 * kVec + 255) / 256;   // elements per thread
   float mrun[kPer], drun[kPer];
   f32x4 orun[kPer];
 #pragma unroll
@@ -936,30 +937,34 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
     }
     __syncthreads();
     const int cnt = s_nslot;
+    // two parts at a time (a cut item has two in most cases): every load of
+    // the thread's elements is issued before the first merge (addresses
+    // clamped into the item's rows)
+    for (int k0 = 0; k0 < cnt; k0 += 2) {
+      float2 ml[kPer][2];
+      f32x4 o[kPer][2];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int idx = tid + i * 256;
-      if (idx >= rows * kVec) break;
-      const int m = idx / kVec;
-      const int d = (idx % kVec) * 4;
-      // two parts at a time: both parts' loads are issued before their merge
-      for (int k0 = 0; k0 < cnt; k0 += 2) {
-        float2 ml[2];
-        f32x4 o[2];
+      for (int i = 0; i < kPer; ++i) {
+        const int idx = min(tid + i * 256, nel - 1);
+        const int m = idx / kVec;
+        const int d = (idx % kVec) * 4;
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const int64_t slot = s_slot[min(k0 + u, cnt - 1)];
-          ml[u] = p.part_ml[slot * (MT * 16) + m];
-          o[u] = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
+          ml[i][u] = p.part_ml[slot * (MT * 16) + m];
+          o[i][u] = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
         }
+      }
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          if (k0 + u >= cnt || ml[u].x == -INFINITY) continue;   // no visible token there
-          const float mx = fmaxf(mrun[i], ml[u].x);
+          if (k0 + u >= cnt || ml[i][u].x == -INFINITY) continue;   // no visible token there
+          const float mx = fmaxf(mrun[i], ml[i][u].x);
           const float a = mrun[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun[i] - mx);
-          const float b = __builtin_amdgcn_exp2f(ml[u].x - mx);
-          orun[i] = a * orun[i] + b * o[u];
-          drun[i] = a * drun[i] + b * ml[u].y;
+          const float b = __builtin_amdgcn_exp2f(ml[i][u].x - mx);
+          orun[i] = a * orun[i] + b * o[i][u];
+          drun[i] = a * drun[i] + b * ml[i][u].y;
           mrun[i] = mx;
         }
       }
@@ -969,7 +974,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
     const int idx = tid + i * 256;
-    if (idx >= rows * kVec) break;
+    if (idx >= nel) continue;
     const int m = idx / kVec;
     const int d = (idx % kVec) * 4;
     const float inv = drun[i] > 0.f ? 1.f / drun[i] : 0.f;
