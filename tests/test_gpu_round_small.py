@@ -135,6 +135,29 @@ def test_ragged_batch_of_64(device):
         _check_all(cfg, meta, device, waves=36, fused=fused)
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_largest_batch(device, fused):
+    """The largest batch the attention entry points take (8192 requests): the
+    work order and span prefix of the whole batch sit in LDS.  Short contexts
+    keep the oracle quick; every request is checked."""
+    bs = 8192
+    rng = np.random.default_rng(21)
+    lens = rng.integers(1, 48, bs)
+    depth = np.minimum(rng.integers(0, 4, bs), lens - 1)
+    cfg = custom_config(seed=22, bs=bs, num_q_heads=4, num_kv_heads=2, head_dim=64, vocab=0,
+                        n_arriving=int(0.3 * bs), pool_blocks=None, k_lo=0, k_hi=3)
+    meta = make_meta(cfg, seq_lens=lens, depth=depth)
+    _check_all(cfg, meta, device, fused=fused)
+    # one request more than the limit is refused before any launch
+    q = torch.zeros((bs + 1, 4, 64), dtype=torch.bfloat16, device=device)
+    with pytest.raises(nsd.NsdError):
+        nsd.verify_attention(q, torch.zeros((4, 2, 8, 16, 8), dtype=torch.bfloat16, device=device),
+                             torch.zeros((4, 2, 64, 16), dtype=torch.bfloat16, device=device),
+                             torch.zeros((bs + 1, 1), dtype=torch.int32, device=device),
+                             torch.ones(bs + 1, dtype=torch.int32, device=device),
+                             torch.arange(bs + 2, dtype=torch.int32, device=device), 1, 1)
+
+
 def test_multi_layer_gather_subrange(device):
     cfg = custom_config(seed=3, num_layers=3)
     meta = make_meta(cfg)
