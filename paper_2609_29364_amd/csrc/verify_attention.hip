@@ -33,8 +33,8 @@
 // * Software pipeline: within an item K(j+1) is requested as soon as S(j)
 //   consumed K(j) and V(j+1) as soon as PV(j) consumed V(j); across items the
 //   next item's first span is requested during the current item's last span
-//   (and, where registers allow, its Q is fetched one item ahead), so a wave
-//   never drains its K/V loads at an item boundary.  Block ids are wave-uniform scalar loads; every vector
+//   (without fusion, together with its Q), so a wave never drains its K/V
+//   loads at an item boundary.  Block ids are wave-uniform scalar loads; every vector
 //   load inside a loop is unconditional (a conditional load makes the
 //   compiler wait for all outstanding loads at the join).
 // * Load balance (stream-K): the spans of all (request, KV head) items are cut
@@ -376,9 +376,11 @@ __device__ inline void store_v(const VOps<D, NB>& o, const Params& p, const Span
   }
 }
 
-// Q operands of item it for this lane's rows (garbage past the item's rows,
-// zeroed when staged).  Addresses are clamped into the Q tensor so the loads
-// are unconditional.
+// Q operands of item it for this lane's rows.  Rows past the item's rows load
+// its last row again (addresses clamped into the Q tensor, so the loads are
+// unconditional): the tile products never mix rows (a row's scores, softmax
+// and output column depend on that row's Q alone), and such rows are never
+// stored, so they need no masking.
 template <int D, int MT>
 __device__ inline void load_q(QOps<MT, D>& o, const Params& p, const Item& it, int total_q,
                               int lane) {
@@ -393,18 +395,6 @@ __device__ inline void load_q(QOps<MT, D>& o, const Params& p, const Item& it, i
     const uint16_t* src = p.q + ((int64_t)qrow * p.num_q_heads + h) * D;
 #pragma unroll
     for (int kk = 0; kk < D / 32; ++kk) o.q[mt][kk] = *(const u32x4*)(src + kk * 32 + grp * 8);
-  }
-}
-
-// Rows past the item's rows become zeros once their Q is current.
-template <int D, int MT>
-__device__ inline void mask_q(QOps<MT, D>& o, const Item& it, int lane) {
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const bool valid = mt * 16 + (lane & 15) < it.rows;
-#pragma unroll
-    for (int kk = 0; kk < D / 32; ++kk)
-      o.q[mt][kk] = valid ? o.q[mt][kk] : u32x4{0, 0, 0, 0};
   }
 }
 
@@ -536,18 +526,23 @@ __device__ inline void span_pv(const VOps<D, NB>& v, const SpanRef<NB>& s, int L
 // has consumed are refilled at once with span nj of item nit (whose table
 // entries were requested before this step, so their latency hides behind the
 // score products); with STORE (fused variant, arriving item) the loaded tiles
-// are first written to the pool.
-template <int D, int MT, int NB, bool FUSE, bool STORE>
+// are first written to the pool.  With NEXTQ (the item's last span; nit is
+// the next item) the Q registers, free once the scores are formed, are
+// refilled with nit's Q before its first K/V loads are issued: the loads
+// complete in order, so waiting for that K also covers Q, and the switch to
+// the next item waits for nothing.
+template <int D, int MT, int NB, bool FUSE, bool STORE, bool NEXTQ>
 __device__ inline void span_step(KOps<D, NB>& kr, VOps<D, NB>& vr, SpanRef<NB>& cur,
                                  const Item& nit, int nj, const SpanIds<NB>& nids,
-                                 const QOps<MT, D>& q, const Params& p, Acc<D, MT>& a, int win,
-                                 int L, int lane) {
+                                 QOps<MT, D>& q, const Params& p, Acc<D, MT>& a, int win, int L,
+                                 int total_q, int lane) {
   f32x4 st[NB][MT];
   span_scores<D, MT, NB>(kr, q, st);
   if constexpr (STORE) store_k<D, NB>(kr, p, cur, lane);
   // keep the next span's address arithmetic (and the wait for its table
   // entries) behind the score products
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (NEXTQ) load_q<D, MT>(q, p, nit, total_q, lane);
   const SpanRef<NB> nr = make_ref<NB, FUSE>(p, nit, nj, nids);
   load_k<D, NB>(kr, nr, lane);
   bf16x8 pop[NB / 2][MT];
@@ -675,16 +670,20 @@ template <int D, int MT, int NB, bool FUSE, bool ARR>
 __device__ inline void run_item(const Params& p, const int32_t* __restrict__ block_table,
                                 const int32_t* __restrict__ stage_table, const Item& it,
                                 const Item& next, KOps<D, NB>& kreg, VOps<D, NB>& vreg,
-                                SpanRef<NB>& cur, const QOps<MT, D>& q, Acc<D, MT>& a,
+                                SpanRef<NB>& cur, QOps<MT, D>& q, Acc<D, MT>& a, int total_q,
                                 int lane) {
   SpanIds<NB> ids = ids_after<NB, FUSE>(p, block_table, stage_table, it, next, it.j0);
   for (int j = it.j0; j + 1 < it.j1; ++j) {
     const SpanIds<NB> ids2 = ids_after<NB, FUSE>(p, block_table, stage_table, it, next, j + 1);
-    span_step<D, MT, NB, FUSE, ARR>(kreg, vreg, cur, it, j + 1, ids, q, p, a, it.win, it.L, lane);
+    span_step<D, MT, NB, FUSE, ARR, false>(kreg, vreg, cur, it, j + 1, ids, q, p, a, it.win, it.L,
+                                           total_q, lane);
     ids = ids2;
   }
-  span_step<D, MT, NB, FUSE, ARR>(kreg, vreg, cur, next, next.j0, ids, q, p, a, it.win, it.L,
-                                  lane);
+  // the last span also brings in the next item's first K/V, and (without
+  // fusion) its Q; the fused tile has no registers to spare there (its Q
+  // loaded here spilled and cost 4 %), so it loads Q at the switch
+  span_step<D, MT, NB, FUSE, ARR, !FUSE>(kreg, vreg, cur, next, next.j0, ids, q, p, a, it.win,
+                                         it.L, total_q, lane);
 }
 
 // One range [s, s1) of global spans, range id rid: online softmax over every
@@ -718,12 +717,12 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
   Item next = following(it);
   bool more = next.base != it.base;
 
-  // Q of the next item is fetched one item ahead when the tile leaves room
-  // for a second copy (PREQ); larger tiles, and the fused variant (whose
-  // store path needs the registers: a second copy spilled to scratch memory
-  // and cost 5 % of the pass), fetch it at the switch.
-  constexpr bool PREQ = D * MT <= 256 && !FUSE;
-  QOps<MT, D> qc, qn;
+  // the first item's Q; without fusion each later item's Q comes with its
+  // first K/V loads, during the previous item's last span (one set of Q
+  // registers: a second copy for a prefetch one item ahead spilled in the
+  // fused tile, and moving it between register files made the wave wait for
+  // all its loads at every item switch)
+  QOps<MT, D> qc;
   load_q<D, MT>(qc, p, it, total_q, lane);
   SpanRef<NB> cur =
       make_ref<NB, FUSE>(p, it, it.j0, load_ids<NB, FUSE>(p, block_table, stage_table, it, it.j0));
@@ -731,27 +730,23 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
   VOps<D, NB> vreg;
   load_k<D, NB>(kreg, cur, lane);
   load_v<D, NB>(vreg, cur, lane);
-  mask_q<D, MT>(qc, it, lane);
-  if constexpr (PREQ) load_q<D, MT>(qn, p, next, total_q, lane);
   while (true) {
     Acc<D, MT> a;
     init_acc<D, MT>(a, p, it, lane);
     if (FUSE && it.arriving)
       run_item<D, MT, NB, FUSE, true>(p, block_table, stage_table, it, next, kreg, vreg, cur,
-                                      qc, a, lane);
+                                      qc, a, total_q, lane);
     else
       run_item<D, MT, NB, FUSE, false>(p, block_table, stage_table, it, next, kreg, vreg, cur,
-                                       qc, a, lane);
+                                       qc, a, total_q, lane);
     finish_item<D, MT>(p, a, it, rid, lane);
     if (!more) break;
-    // switch to the next item
-    if constexpr (PREQ) qc = qn;
-    else load_q<D, MT>(qc, p, next, total_q, lane);
-    mask_q<D, MT>(qc, next, lane);
+    // switch to the next item (its first span, and Q without fusion, are
+    // already requested)
+    if constexpr (FUSE) load_q<D, MT>(qc, p, next, total_q, lane);
     it = next;
     next = following(it);
     more = next.base != it.base;
-    if constexpr (PREQ) load_q<D, MT>(qn, p, next, total_q, lane);
   }
 }
 
