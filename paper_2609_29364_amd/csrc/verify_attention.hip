@@ -34,9 +34,9 @@
 //   consumed K(j) and V(j+1) as soon as PV(j) consumed V(j); across items the
 //   next item's first span is requested during the current item's last span
 //   (without fusion, together with its Q), so a wave never drains its K/V
-//   loads at an item boundary.  Block ids are wave-uniform scalar loads; every vector
-//   load inside a loop is unconditional (a conditional load makes the
-//   compiler wait for all outstanding loads at the join).
+//   loads at an item boundary.  Block ids are wave-uniform scalar loads;
+//   every vector load inside a loop is unconditional (a conditional load
+//   makes the compiler wait for all outstanding loads at the join).
 // * Load balance (stream-K): the spans of all (request, KV head) items are cut
 //   into as many equal contiguous ranges as the device keeps waves resident,
 //   whatever the spread of context lengths.  The fused variant cuts the
