@@ -48,6 +48,13 @@
 //   Items cut by a range boundary leave partials that a small second kernel
 //   merges in range order (deterministic, no atomics in the arithmetic); all
 //   other items are written directly.
+// * No stores while the K/V stream runs: stores retire through the same
+//   in-order vector-memory counter as the loads, and a store's
+//   acknowledgement comes late under a full read stream, so every later load
+//   wait would also wait for it.  A finished item's output rows (or its
+//   partial) go to the wave's LDS buffer, which is written out, in whole
+//   rows, when it is full and when the wave's work ends.  (The fused
+//   variant's own tile stores are the preparation itself and stay in line.)
 // * Masked tokens (past a query's position, past L_r, or in a block whose id
 //   is out of range) are removed by selection: scores become -inf and V
 //   elements past L_r are zeroed, so NaN-filled unused slots never leak.
@@ -70,9 +77,15 @@ constexpr int kBlock = 16;        // token slots per KV block
 constexpr int kMaxRows = 64;      // (Hq/Hkv) * max_q_per_seq limit
 constexpr int kMaxBatch = 8192;   // the span prefix of the batch lives in LDS
 
-// Blocks per main-loop step for a (head_dim, row tiles) instantiation: four
-// where the registers of two extra K/V tiles fit beside the accumulators.
-__host__ __device__ constexpr int span_blocks(int d, int mt) { return d * mt <= 256 ? 4 : 2; }
+// Blocks per main-loop step for a (head_dim, row tiles, fused) instantiation:
+// four where the registers of two extra K/V tiles fit beside the
+// accumulators.  The fused tile also holds its store path: with four blocks
+// and more than one 16-row tile at head_dim 128 it ran out of registers and
+// reloaded a spilled lane offset before every span's loads (waiting for all
+// of them), so it takes two.
+__host__ __device__ constexpr int span_blocks(int d, int mt, bool fuse) {
+  return (fuse && d * mt > 128) ? 2 : (d * mt <= 256 ? 4 : 2);
+}
 
 struct Params {
   const uint16_t* q;
@@ -101,6 +114,8 @@ struct Params {
   int32_t max_q;
   int32_t max_seq_len;
   int32_t num_waves;
+  int32_t out_off;         // dynamic LDS: byte offset of the output buffers
+  int32_t out_cap;         // bytes of each wave's output buffer
   int32_t w_even;          // relative range length of waves on even XCDs
   int32_t w_odd, w_odd_b;  // ... on odd XCDs, resident / arriving segment
   float scale_log2;  // softmax scale * log2(e)
@@ -566,43 +581,125 @@ __device__ inline void init_acc(Acc<D, MT>& a, const Params& p, const Item& it, 
   }
 }
 
-// Finish item it: a whole item is normalised and written to the output; an
+// Results leave the wave through LDS.  Stores share the in-order
+// vector-memory counter with the K/V loads, so a store issued while loads
+// stream makes every later load wait also wait for the store, whose
+// acknowledgement, under a full read stream, comes late: storing each item's
+// rows when it finishes cost 12 % of the pass.  Instead each finished 16-row
+// tile is appended to the wave's LDS buffer (a 16-byte header, then the rows,
+// padded by 16 bytes so the 16 rows of a column fall in different banks) and
+// the buffer is written out when it is full and when the wave's work ends.
+struct OutBuf {
+  char* base;   // this wave's LDS buffer
+  int cap;      // its bytes
+  int used;     // bytes holding records (wave-uniform)
+};
+
+constexpr int kOutO = 1;   // record of normalised bf16 output rows
+constexpr int kOutP = 2;   // record of fp32 partial rows (and their max, sum)
+
+// Bytes of one record (16-byte aligned): header, rows, and for partials each
+// row's (max, sum).
+template <int D>
+__host__ __device__ constexpr int out_record_bytes(int kind, int nrows) {
+  return (kind == kOutO ? 16 + nrows * (D * 2 + 16)
+                        : 16 + nrows * (D * 4 + 16) + nrows * 8 + 15) / 16 * 16;
+}
+
+// Ordering of the wave's LDS writes before its reads of other lanes' data,
+// and of those reads before the buffer is written again: a compiler memory
+// barrier and a wait for the wave's LDS operations.
+__device__ inline void lds_fence() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Write out every record of the buffer: each row with whole 16-byte chunks,
+// the lanes of a row contiguous.
+template <int D, int MT>
+__device__ inline void out_flush(const Params& p, OutBuf& ob, int lane) {
+  lds_fence();
+  int off = 0;
+  while (off < ob.used) {
+    // header: kind, (KV head << 16) | rows, first row, qo (output) or slot (partial)
+    const int4 h = *(const int4*)(ob.base + off);
+    const int kind = uniform(h.x), nrows = uniform(h.y), m0 = uniform(h.z), key = uniform(h.w);
+    const char* rows = ob.base + off + 16;
+    if (kind == kOutO) {
+      const int qo = key;
+      const int gg = nrows >> 16, nr = nrows & 0xffff;
+      constexpr int RS = D * 2 + 16, CPR = D / 8, RPI = 64 / CPR;
+      const int c = lane % CPR, rr = lane / CPR;
+      for (int r0 = 0; r0 < nr; r0 += RPI) {
+        const int r = r0 + rr;
+        if (r < nr) {
+          const u32x4 v = *(const u32x4*)(rows + r * RS + c * 16);
+          const int m = m0 + r;
+          const int j = m / p.group, hh = gg * p.group + m % p.group;
+          *(u32x4*)(p.out + ((int64_t)(qo + j) * p.num_q_heads + hh) * D + c * 8) = v;
+        }
+      }
+      off += out_record_bytes<D>(kOutO, nr);
+    } else {
+      const int64_t slot = key;
+      const int nr = nrows & 0xffff;
+      constexpr int RS = D * 4 + 16, CPR = D / 4, RPI = 64 / CPR;
+      const int c = lane % CPR, rr = lane / CPR;
+      for (int r0 = 0; r0 < nr; r0 += RPI) {
+        const int r = r0 + rr;
+        if (r < nr)
+          *(f32x4*)(p.part_o + (slot * (MT * 16) + m0 + r) * D + c * 4) =
+              *(const f32x4*)(rows + r * RS + c * 16);
+      }
+      if (lane < nr)
+        p.part_ml[slot * (MT * 16) + m0 + lane] = *(const float2*)(rows + nr * RS + lane * 8);
+      off += out_record_bytes<D>(kOutP, nr);
+    }
+  }
+  ob.used = 0;
+  lds_fence();
+}
+
+// Finish item it: a whole item is normalised and becomes output rows; an
 // item cut by a range boundary leaves its partial in the range's head slot
 // (the item began in an earlier range) or tail slot (it continues later).
+// Both go to the wave's LDS buffer, one record per 16-row tile.
 template <int D, int MT>
 __device__ inline void finish_item(const Params& p, Acc<D, MT>& a, const Item& it, int64_t rid,
-                                   int lane) {
-  const int grp = lane >> 4;
+                                   int lane, OutBuf& ob) {
+  const int grp = lane >> 4, row = lane & 15;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) a.l[mt] = wave_sum_groups(a.l[mt]);
-  if (it.j0 == 0 && it.j1 == it.n) {
+  const bool whole = it.j0 == 0 && it.j1 == it.n;
+  const int slot = (int)(2 * rid + (it.j0 > 0 ? 0 : 1));
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = mt * 16 + (lane & 15);
-      if (m >= it.rows) continue;
-      const int j = m / p.group;
-      const int h = it.g * p.group + m % p.group;
-      const float inv = a.l[mt] > 0.f ? 1.f / a.l[mt] : 0.f;
-      uint16_t* dst = p.out + ((int64_t)(it.qo + j) * p.num_q_heads + h) * D + grp * 4;
+  for (int mt = 0; mt < MT; ++mt) {
+    if (mt * 16 >= it.rows) break;
+    const int nr = min(16, it.rows - mt * 16);
+    const int kind = whole ? kOutO : kOutP;
+    const int need = out_record_bytes<D>(kind, nr);
+    if (ob.used + need > ob.cap) out_flush<D, MT>(p, ob, lane);
+    char* rec = ob.base + ob.used;
+    if (lane == 0)
+      *(int4*)rec = whole ? int4{kOutO, (it.g << 16) | nr, mt * 16, it.qo}
+                          : int4{kOutP, nr, mt * 16, slot};
+    char* rows = rec + 16;
+    if (row < nr) {
+      if (whole) {
+        const float inv = a.l[mt] > 0.f ? 1.f / a.l[mt] : 0.f;
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const bf16x2 lo = {(__bf16)(a.o[mt][dt][0] * inv), (__bf16)(a.o[mt][dt][1] * inv)};
-        const bf16x2 hi = {(__bf16)(a.o[mt][dt][2] * inv), (__bf16)(a.o[mt][dt][3] * inv)};
-        *(u32x2*)(dst + dt * 16) = u32x2{__builtin_bit_cast(uint32_t, lo),
-                                         __builtin_bit_cast(uint32_t, hi)};
+        for (int dt = 0; dt < D / 16; ++dt) {
+          const bf16x2 lo = {(__bf16)(a.o[mt][dt][0] * inv), (__bf16)(a.o[mt][dt][1] * inv)};
+          const bf16x2 hi = {(__bf16)(a.o[mt][dt][2] * inv), (__bf16)(a.o[mt][dt][3] * inv)};
+          *(u32x2*)(rows + row * (D * 2 + 16) + (dt * 16 + grp * 4) * 2) =
+              u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+        }
+      } else {
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt)
+          *(f32x4*)(rows + row * (D * 4 + 16) + (dt * 16 + grp * 4) * 4) = a.o[mt][dt];
+        if (grp == 0)
+          *(float2*)(rows + nr * (D * 4 + 16) + row * 8) = make_float2(a.m[mt], a.l[mt]);
       }
     }
-  } else {
-    const int64_t slot = 2 * rid + (it.j0 > 0 ? 0 : 1);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = mt * 16 + (lane & 15);
-      if (m >= it.rows) continue;   // stores of unused rows cost far more than the branch
-      float* dst = p.part_o + (slot * (MT * 16) + m) * D + grp * 4;
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) *(f32x4*)(dst + dt * 16) = a.o[mt][dt];
-      if (grp == 0) p.part_ml[slot * (MT * 16) + m] = make_float2(a.m[mt], a.l[mt]);
-    }
+    ob.used += need;
   }
 }
 
@@ -694,7 +791,7 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
                               const int32_t* __restrict__ seq_lens,
                               const int32_t* __restrict__ q_indptr, const uint32_t* pre,
                               const uint16_t* order, int total_q, int64_t rid, int64_t s,
-                              int64_t s1, int lane) {
+                              int64_t s1, int lane, OutBuf& ob) {
   const int hkv = p.num_kv_heads;
   const int pos0 = uniform(find_position(pre, p.bs, hkv, s));
   const int r0 = uniform(request_at<FUSE>(order, pos0));
@@ -739,7 +836,7 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
     else
       run_item<D, MT, NB, FUSE, false>(p, block_table, stage_table, it, next, kreg, vreg, cur,
                                        qc, a, total_q, lane);
-    finish_item<D, MT>(p, a, it, rid, lane);
+    finish_item<D, MT>(p, a, it, rid, lane, ob);
     if (!more) break;
     // switch to the next item (its first span, and Q without fusion, are
     // already requested)
@@ -777,11 +874,12 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
                              const int32_t* __restrict__ stage_table,
                              const int32_t* __restrict__ seq_lens,
                              const int32_t* __restrict__ q_indptr) {
-  constexpr int NB = span_blocks(D, MT);
+  constexpr int NB = span_blocks(D, MT, FUSE);
   extern __shared__ uint32_t s_pre[];   // [bs + 1] span prefix by position, then uint16 order[bs]
   uint16_t* s_order = (uint16_t*)(s_pre + p.bs + 1);
   __shared__ uint32_t s_wsum[3][4];
   __shared__ uint32_t s_red[4];
+
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = uniform(tid >> 6);
@@ -857,6 +955,11 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
   const int64_t ta = hkv * s_pre[n_res], tb = hkv * s_pre[p.bs] - ta;
   const Ranges ra(ta, p.num_waves, p.w_even, p.w_odd), rb(tb, p.num_waves, p.w_even, p.w_odd_b);
   const int64_t rid = (int64_t)blockIdx.x * 4 + wave;
+  // this wave's output buffer follows the span prefix and the work order
+  OutBuf ob;
+  ob.base = (char*)s_pre + p.out_off + wave * p.out_cap;
+  ob.cap = p.out_cap;
+  ob.used = 0;
   // resident range first, then the arriving range (writes last)
 #pragma unroll 1
   for (int k = 0; k < (FUSE ? 2 : 1); ++k) {
@@ -867,17 +970,17 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
     if (b < e)
       process_range<D, MT, NB, FUSE>(p, block_table, stage_table, seq_lens, q_indptr, s_pre,
                                      s_order, total_q, seg_b ? p.num_waves + rid : rid, b, e,
-                                     lane);
+                                     lane, ob);
   }
+  out_flush<D, MT>(p, ob, lane);
 }
 
 // Merge the partials of every item that a range boundary cut, in range order
 // (deterministic, no atomics).  One workgroup per (KV head, request); the
 // ranges holding the item's spans and their partial slots are found once per
 // workgroup.
-template <int D, int MT>
+template <int D, int MT, int NB>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
-  constexpr int NB = span_blocks(D, MT);
   __shared__ int64_t s_slot[256];   // partial slots of the item, in range order
   __shared__ int s_nslot;
   const int g = blockIdx.x;
@@ -1008,7 +1111,7 @@ const void* kernel_for(int d, int mt) {
 struct Plan {
   int mt;            // 16-row tiles
   int num_waves;     // W: resident waves of the launch
-  size_t lds_bytes;  // dynamic LDS: the span prefix
+  size_t lds_bytes;  // dynamic LDS of the span prefix and work order
   size_t prefix_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
 };
 
@@ -1057,7 +1160,8 @@ void launch(const Params& p, int bs, size_t lds_bytes, hipStream_t stream) {
   hipLaunchKernelGGL((verify_attention_kernel<D, MT, FUSE>), dim3(p.num_waves / 4), dim3(256),
                      lds_bytes, stream, p, p.block_table, p.stage_table, p.seq_lens,
                      p.q_indptr);
-  hipLaunchKernelGGL((combine_kernel<D, MT>), dim3(p.num_kv_heads, bs), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL((combine_kernel<D, MT, span_blocks(D, MT, FUSE)>), dim3(p.num_kv_heads, bs),
+                     dim3(256), 0, stream, p);
 }
 
 template <int D, bool FUSE>
@@ -1110,17 +1214,26 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   if (!workspace || workspace_bytes < pl.ws_bytes)
     return fail(NSD_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn,
                 pl.ws_bytes, workspace ? workspace_bytes : (size_t)0);
+  // dynamic LDS: the span prefix and work order, then one output buffer per
+  // wave taking the rest of what a workgroup may have (at least one record)
   int dev = 0, lds_max = 0;
   hipFuncAttributes fa;
   const void* kfn = fuse ? kernel_for<true>(head_dim, pl.mt) : kernel_for<false>(head_dim, pl.mt);
-  if (hipGetDevice(&dev) == hipSuccess &&
-      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
-          hipSuccess &&
-      hipFuncGetAttributes(&fa, kfn) == hipSuccess &&
-      fa.sharedSizeBytes + pl.lds_bytes > (size_t)lds_max)
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+          hipSuccess ||
+      hipFuncGetAttributes(&fa, kfn) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(NSD_ERR_HIP, "%s: the device's LDS size could not be queried", fn);
+  }
+  const size_t pre_bytes = (pl.lds_bytes + 15) / 16 * 16;
+  const size_t fixed = fa.sharedSizeBytes + pre_bytes;
+  const size_t per_wave = (size_t)lds_max > fixed ? ((size_t)lds_max - fixed) / 4 / 16 * 16 : 0;
+  const size_t min_cap = head_dim == 64 ? out_record_bytes<64>(kOutP, 16)
+                                        : out_record_bytes<128>(kOutP, 16);
+  if (per_wave < min_cap)
     return fail(NSD_ERR_UNSUPPORTED, "%s: bs=%d needs %zu bytes of LDS, %d available", fn, bs,
-                fa.sharedSizeBytes + pl.lds_bytes, lds_max);
-  (void)hipGetLastError();
+                fixed + 4 * min_cap, lds_max);
 
   Params p;
   p.q = (const uint16_t*)q;
@@ -1157,14 +1270,17 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   p.w_odd = 94;
   p.w_odd_b = 91;
   p.scale_log2 = scale * 1.4426950408889634f;
+  p.out_off = (int32_t)pre_bytes;
+  p.out_cap = (int32_t)per_wave;
+  const size_t lds_bytes = pre_bytes + 4 * per_wave;
 
   clear_stale_error();
   if (fuse) {
-    if (head_dim == 64) launch_d<64, true>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
-    else launch_d<128, true>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
+    if (head_dim == 64) launch_d<64, true>(p, pl.mt, bs, lds_bytes, (hipStream_t)stream);
+    else launch_d<128, true>(p, pl.mt, bs, lds_bytes, (hipStream_t)stream);
   } else {
-    if (head_dim == 64) launch_d<64, false>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
-    else launch_d<128, false>(p, pl.mt, bs, pl.lds_bytes, (hipStream_t)stream);
+    if (head_dim == 64) launch_d<64, false>(p, pl.mt, bs, lds_bytes, (hipStream_t)stream);
+    else launch_d<128, false>(p, pl.mt, bs, lds_bytes, (hipStream_t)stream);
   }
   return check_launch(fn);
 }
