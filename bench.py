@@ -145,7 +145,9 @@ def practical_ceiling(dev, read_bytes, write_bytes, reps=7, placement="end"):
     placement of the written tiles (same bytes): "end" the last share of every
     wave's sequence (the fused pass's order); "spread" runs of 40 steps (one
     request's item) scattered through every wave's sequence; "waves" every tile
-    of a share of the waves, the others only reading."""
+    of a share of the waves, the others only reading; "writer" the same number
+    of tiles stored by a fifth wave per workgroup that does not read (the four
+    readers only read), which also reports the writes alone."""
     import ctypes
     import torch
     from paper_2609_29364_amd.build import PROBE_LIB_PATH
@@ -154,6 +156,10 @@ def practical_ceiling(dev, read_bytes, write_bytes, reps=7, placement="end"):
                                     ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                     ctypes.c_void_p]
+    lib.nsd_probe_tiles_writer.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                           ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_void_p, ctypes.c_void_p]
     tile = 4096
     waves = 4 * torch.cuda.get_device_properties(dev).multi_processor_count
     steps = max(2, int(read_bytes / (waves * 4 * tile)))
@@ -169,7 +175,7 @@ def practical_ceiling(dev, read_bytes, write_bytes, reps=7, placement="end"):
     # wave's sequence
     frac = write_bytes / read_bytes if read_bytes else 0.0
     step_in_wave = (np.arange(n) // 4) % steps
-    if placement == "end":
+    if placement in ("end", "writer"):
         written = step_in_wave >= steps - int(round(frac * steps))
     elif placement == "spread":
         written = ((np.arange(n) // 4 // 40) * 7919 % 1000) < frac * 1000
@@ -179,41 +185,60 @@ def practical_ceiling(dev, read_bytes, write_bytes, reps=7, placement="end"):
         raise ValueError(placement)
     dids = np.where(written, rng.permutation(n), -1).astype(np.int32)
     dids_d = torch.as_tensor(dids, device=dev)
+    # "writer": the written tiles' destinations dealt to the workgroups' writer
+    # waves in turn, -1 padding
+    wgs = waves // 4
+    wdst = dids[dids >= 0]
+    write_per = max(1, -(-len(wdst) // wgs))
+    wl = np.full(wgs * write_per, -1, np.int32)
+    wl[:len(wdst)] = wdst
+    wl_d = torch.as_tensor(wl.reshape(write_per, wgs).T.copy().reshape(-1), device=dev)
     stream = torch.cuda.current_stream(dev)
     sp = ctypes.c_void_p(stream.cuda_stream)
 
-    def run(with_writes):
-        st = lib.nsd_probe_tiles(src.data_ptr(), src_tiles, dst.data_ptr(), n, ids.data_ptr(),
-                                 dids_d.data_ptr() if with_writes else None, waves, steps,
-                                 sink.data_ptr(), sp)
+    def run(kind):
+        if placement == "writer" and kind != "read":
+            st = lib.nsd_probe_tiles_writer(src.data_ptr(), src_tiles, dst.data_ptr(), n,
+                                            ids.data_ptr(), wl_d.data_ptr(), write_per, waves,
+                                            0 if kind == "write" else steps, sink.data_ptr(), sp)
+        else:
+            st = lib.nsd_probe_tiles(src.data_ptr(), src_tiles, dst.data_ptr(), n,
+                                     ids.data_ptr(), dids_d.data_ptr() if kind == "mix" else None,
+                                     waves, steps, sink.data_ptr(), sp)
         if st != 0:
-            raise RuntimeError(f"nsd_probe_tiles status {st}")
+            raise RuntimeError(f"probe status {st}")
 
     out = {}
-    for key, wr in (("read_only_gbs", False), ("mix_gbs", True)):
-        if wr and not write_bytes:
+    kinds = [("read_only_gbs", "read"), ("mix_gbs", "mix")]
+    if placement == "writer":
+        kinds.append(("write_only_gbs", "write"))
+    for key, kind in kinds:
+        if kind != "read" and not write_bytes:
             out[key] = out["read_only_gbs"]
             continue
-        run(wr)
+        run(kind)
         torch.cuda.synchronize()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
         ev[0].record(stream)
         for k in range(reps):
-            run(wr)
+            run(kind)
             ev[k + 1].record(stream)
         torch.cuda.synchronize()
         ms = float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(reps)]))
-        moved = n * tile + (int(written.sum()) * tile if wr else 0)
+        moved = (n * tile if kind != "write" else 0) + \
+            (int(written.sum()) * tile if kind != "read" else 0)
         out[key] = round(moved / (ms * 1e-3) / 1e9, 1)
     out["write_share"] = round(float(written.mean()), 4)
     where = {"end": f"the last {written.mean():.1%} of every wave's tiles",
              "spread": f"{written.mean():.1%} of the tiles, in runs of 40 steps through every "
                        f"wave's sequence",
-             "waves": f"every tile of {written.mean():.1%} of the waves"}[placement]
+             "waves": f"every tile of {written.mean():.1%} of the waves",
+             "writer": f"{written.mean():.1%} of the tiles, by a fifth wave per workgroup "
+                       f"that does not read"}[placement]
     out["pattern"] = (f"random 4 KiB tiles, {waves} persistent waves, up to 32 KiB in flight "
                       f"per wave, {n * tile / 1e9:.2f} GB read"
                       + (f", {where} written back" if write_bytes else ""))
-    del src, dst, sink, ids, dids_d
+    del src, dst, sink, ids, dids_d, wl_d
     torch.cuda.empty_cache()
     return out
 
@@ -780,7 +805,7 @@ def ceiling_bench(args):
     w = alg["gather"] // 2
     res = {"mode": "ceiling", "workload": cfg.name, "read_bytes": alg["fused"] - w,
            "write_bytes": w}
-    for placement in ("end", "spread", "waves"):
+    for placement in ("end", "spread", "waves", "writer"):
         res[placement] = practical_ceiling(dev, alg["fused"] - w, w, placement=placement)
     print(json.dumps(res), flush=True)
 

@@ -36,6 +36,22 @@ int32_t nsd_probe_tiles(const void* src, int64_t src_tiles, void* dst, int64_t d
                         const int32_t* ids, const int32_t* dst_ids, int32_t waves,
                         int32_t steps, void* sink, void* stream);
 
+/*
+ * The same reads with the write-back moved to waves that do not read:
+ * waves / 4 workgroups of five waves (one workgroup per CU), waves 0-3 of
+ * workgroup k reading as nsd_probe_tiles' waves 4k..4k+3 do (dst_ids NULL),
+ * and wave 4 storing, from registers, the tiles write_ids[k * write_per ..
+ * (k + 1) * write_per) of `dst` (entries outside [0, dst_tiles) skipped).
+ * Separates the cost of mixing reads and writes in the memory system from
+ * the cost of stores issued among a wave's loads.  steps = 0 gives the
+ * writes alone (src and ids may then be NULL).
+ *
+ * write_ids: int32 [waves / 4 * write_per]; other arguments as above.
+ */
+int32_t nsd_probe_tiles_writer(const void* src, int64_t src_tiles, void* dst, int64_t dst_tiles,
+                               const int32_t* ids, const int32_t* write_ids, int32_t write_per,
+                               int32_t waves, int32_t steps, void* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -22,19 +22,16 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 constexpr int kTileVec = 4096 / (64 * 16);   // 16-byte loads per lane per 4 KiB tile
 constexpr int kGroup = 4;                     // tiles per group; two groups in flight
 
-// Wave w streams tiles ids[w*steps*G .. (w+1)*steps*G) in groups of G, the
-// next group requested before the current one is consumed.  A tile whose
-// dst_ids entry is >= 0 is stored to that destination tile.
+// One wave streams `steps` groups of G tiles, ids wid[0 .. steps*G), the next
+// group requested before the current one is consumed.  With STORE, a tile
+// whose wdst entry is in [0, dst_tiles) is stored to that destination tile
+// right after it is used.
 template <bool STORE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
-void tiles_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
-                  int64_t src_tiles, int64_t dst_tiles, const int32_t* __restrict__ ids,
-                  const int32_t* __restrict__ dst_ids, int32_t steps,
-                  u32x4* __restrict__ sink) {
-  const int lane = threadIdx.x & 63;
-  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int32_t* wid = ids + wave * steps * kGroup;
-  const int32_t* wdst = STORE ? dst_ids + wave * steps * kGroup : nullptr;
+__device__ inline void stream_tiles(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                    int64_t src_tiles, int64_t dst_tiles,
+                                    const int32_t* __restrict__ wid,
+                                    const int32_t* __restrict__ wdst, int32_t steps, int lane,
+                                    u32x4* __restrict__ sink) {
   u32x4 a[kGroup][kTileVec], b[kGroup][kTileVec];
   u32x4 acc = {0, 0, 0, 0};
   auto load = [&](u32x4(&r)[kGroup][kTileVec], int s) {
@@ -73,7 +70,49 @@ void tiles_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
   }
   if (steps & 1) use(a, steps - 1);
   // keeps the loads alive; the data are never all-ones words in practice
-  if ((acc.x & acc.y & acc.z & acc.w) == 0xffffffffu) sink[wave * 64 + lane] = acc;
+  if ((acc.x & acc.y & acc.z & acc.w) == 0xffffffffu) *sink = acc;
+}
+
+// Wave w streams tiles ids[w*steps*G .. (w+1)*steps*G).
+template <bool STORE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
+void tiles_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                  int64_t src_tiles, int64_t dst_tiles, const int32_t* __restrict__ ids,
+                  const int32_t* __restrict__ dst_ids, int32_t steps,
+                  u32x4* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  stream_tiles<STORE>(src, dst, src_tiles, dst_tiles, ids + wave * steps * kGroup,
+                      STORE ? dst_ids + wave * steps * kGroup : nullptr, steps, lane,
+                      sink + wave * 64 + lane);
+}
+
+// Workgroups of five waves: waves 0-3 only read (reader wave 4k+i of the
+// launch streams tiles ids[(4k+i)*steps*G ...]), wave 4 of workgroup k only
+// writes: the tiles write_ids[k*write_per .. (k+1)*write_per) of dst, from
+// registers (entries outside [0, dst_tiles) are skipped).
+__global__ __launch_bounds__(320) __attribute__((amdgpu_waves_per_eu(2)))
+void writer_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst, int64_t src_tiles,
+                   int64_t dst_tiles, const int32_t* __restrict__ ids,
+                   const int32_t* __restrict__ write_ids, int32_t write_per, int32_t steps,
+                   u32x4* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  if (w == 4) {
+    const int32_t* my = write_ids + (int64_t)blockIdx.x * write_per;
+    const u32x4 v = {(uint32_t)lane, (uint32_t)blockIdx.x, 0u, 0u};
+    for (int i = 0; i < write_per; ++i) {
+      const int64_t d = __builtin_amdgcn_readfirstlane(my[i]);
+      if (d < 0 || d >= dst_tiles) continue;
+      u32x4* q = dst + d * (64 * kTileVec) + lane;
+#pragma unroll
+      for (int k = 0; k < kTileVec; ++k) __builtin_nontemporal_store(v, q + k * 64);
+    }
+    return;
+  }
+  const int64_t wave = (int64_t)blockIdx.x * 4 + w;
+  stream_tiles<false>(src, nullptr, src_tiles, 0, ids + wave * steps * kGroup, nullptr, steps,
+                      lane, sink + wave * 64 + lane);
 }
 
 }  // namespace
@@ -93,5 +132,28 @@ extern "C" int32_t nsd_probe_tiles(const void* src, int64_t src_tiles, void* dst
   else
     hipLaunchKernelGGL(tiles_kernel<false>, grid, block, 0, s, (const u32x4*)src, nullptr,
                        src_tiles, (int64_t)0, ids, nullptr, steps, (u32x4*)sink);
+  return hipGetLastError() == hipSuccess ? 0 : 5;
+}
+
+extern "C" int32_t nsd_probe_tiles_writer(const void* src, int64_t src_tiles, void* dst,
+                                          int64_t dst_tiles, const int32_t* ids,
+                                          const int32_t* write_ids, int32_t write_per,
+                                          int32_t waves, int32_t steps, void* sink,
+                                          void* stream) {
+  if (!dst || !write_ids || !sink || (steps > 0 && (!src || !ids))) return 1;
+  if (waves <= 0 || waves % 4 != 0 || steps < 0 || write_per < 0 || dst_tiles <= 0 ||
+      (steps > 0 && src_tiles <= 0))
+    return 2;
+  // more than half the LDS a workgroup may use, so that one workgroup runs per
+  // CU, as in the attention pass
+  int dev = 0, lds_max = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+          hipSuccess)
+    return 5;
+  const size_t lds = lds_max > 65536 ? (size_t)lds_max / 2 + 4096 : 0;
+  hipLaunchKernelGGL(writer_kernel, dim3(waves / 4), dim3(320), lds, (hipStream_t)stream,
+                     (const u32x4*)src, (u32x4*)dst, src_tiles, dst_tiles, ids, write_ids,
+                     write_per, steps, (u32x4*)sink);
   return hipGetLastError() == hipSuccess ? 0 : 5;
 }

@@ -156,7 +156,7 @@ def test_probe_library_exports_and_validates():
     src = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "nsd_probe.h")).read(),
                  flags=re.S)
     names = sorted(set(re.findall(r"\b(nsd_\w+)\s*\(", src)))
-    assert names == ["nsd_probe_tiles"]
+    assert names == ["nsd_probe_tiles", "nsd_probe_tiles_writer"]
     for name in names:
         assert hasattr(plib, name), name
     f = plib.nsd_probe_tiles
@@ -169,3 +169,14 @@ def test_probe_library_exports_and_validates():
     assert f(fake, 8, None, 0, fake, None, 6, 1, fake, None) == 2        # waves % 4
     assert f(fake, 0, None, 0, fake, None, 4, 1, fake, None) == 2        # empty source
     assert f(fake, 8, None, 0, fake, None, 4, -1, fake, None) == 2       # steps < 0
+    w = plib.nsd_probe_tiles_writer
+    w.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    assert w(fake, 8, None, 8, fake, fake, 1, 4, 1, fake, None) == 1     # no destination
+    assert w(fake, 8, fake, 8, fake, None, 1, 4, 1, fake, None) == 1     # no write list
+    assert w(None, 8, fake, 8, None, fake, 1, 4, 1, fake, None) == 1     # reads without source
+    assert w(fake, 8, fake, 8, fake, fake, 1, 6, 1, fake, None) == 2     # waves % 4
+    assert w(fake, 8, fake, 0, fake, fake, 1, 4, 1, fake, None) == 2     # empty destination
+    assert w(fake, 8, fake, 8, fake, fake, -1, 4, 1, fake, None) == 2    # write_per < 0
+    assert w(fake, 8, fake, 8, fake, fake, 1, 4, -1, fake, None) == 2    # steps < 0
