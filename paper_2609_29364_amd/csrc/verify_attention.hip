@@ -76,6 +76,7 @@ typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 constexpr int kBlock = 16;        // token slots per KV block
 constexpr int kMaxRows = 64;      // (Hq/Hkv) * max_q_per_seq limit
 constexpr int kMaxBatch = 8192;   // the span prefix of the batch lives in LDS
+constexpr int kSpare = -1;        // span index of loads that are never used
 
 // Blocks per main-loop step for a (head_dim, row tiles, fused) instantiation:
 // four where the registers of two extra K/V tiles fit beside the
@@ -307,6 +308,19 @@ template <int NB, bool FUSE>
 __device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
                                        const SpanIds<NB>& ids) {
   SpanRef<NB> s;
+  if (j == kSpare) {   // loads that are never used: block 0's tile, nothing stored
+    const bool arr = FUSE && it.arriving;
+    s.k_src = arr ? p.k_stage : p.k_cache;
+    s.v_src = arr ? p.v_stage : p.v_cache;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      s.ts[b] = it.g;
+      s.td[b] = -1;
+    }
+    s.t = 0;
+    s.bad = 0;
+    return s;
+  }
   s.t = j * NB * kBlock;
   s.bad = 0;
   const int nb = max(1, min(NB, (it.L - s.t + kBlock - 1) / kBlock));
@@ -746,11 +760,14 @@ __device__ inline int find_position(const uint32_t* pre, int bs, int hkv, int64_
   return lo;
 }
 
-// Spans [j0, j1) of one item.  The loads of the item's first span were issued
-// by the caller; during its last span the first span of `next` is requested
-// (when the range ends inside `it`, `next` is `it` and the loads are spare).
-// Table entries of the span after span j of `it`: span j+1, or the first
-// span of `next` when j is the item's last.
+// Span of `next` requested during the last span of `it`: next's first span,
+// or kSpare when the range holds nothing after `it` (next is it).
+__device__ inline int first_or_spare(const Item& it, const Item& next) {
+  return next.base == it.base ? kSpare : next.j0;
+}
+
+// Table entries of the span after span j of `it`: span j+1, or next's first
+// span when j is the item's last (when next is it, unused).
 template <int NB, bool FUSE>
 __device__ inline SpanIds<NB> ids_after(const Params& p, const int32_t* __restrict__ block_table,
                                         const int32_t* __restrict__ stage_table, const Item& it,
@@ -760,8 +777,11 @@ __device__ inline SpanIds<NB> ids_after(const Params& p, const int32_t* __restri
 }
 
 // Spans [j0, j1) of one item.  The loads of the item's first span were issued
-// by the caller; during its last span the first span of `next` is requested
-// (when the range ends inside `it`, `next` is `it` and the loads are spare).
+// by the caller; during its last span the first span of `next` is requested.
+// When the range ends inside `it` (or with it), `next` is `it` and those
+// loads are spare (every vector load of the loop is unconditional): they
+// read block 0's tile of the item's KV head, which every wave's spare loads
+// share, so they come from the L2 rather than HBM.
 // Table entries are fetched one step before the step that uses them.
 template <int D, int MT, int NB, bool FUSE, bool ARR>
 __device__ inline void run_item(const Params& p, const int32_t* __restrict__ block_table,
@@ -779,8 +799,8 @@ __device__ inline void run_item(const Params& p, const int32_t* __restrict__ blo
   // the last span also brings in the next item's first K/V, and (without
   // fusion) its Q; the fused tile has no registers to spare there (its Q
   // loaded here spilled and cost 4 %), so it loads Q at the switch
-  span_step<D, MT, NB, FUSE, ARR, !FUSE>(kreg, vreg, cur, next, next.j0, ids, q, p, a, it.win,
-                                         it.L, total_q, lane);
+  span_step<D, MT, NB, FUSE, ARR, !FUSE>(kreg, vreg, cur, next, first_or_spare(it, next), ids, q,
+                                         p, a, it.win, it.L, total_q, lane);
 }
 
 // One range [s, s1) of global spans, range id rid: online softmax over every
