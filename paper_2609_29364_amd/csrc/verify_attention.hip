@@ -308,20 +308,9 @@ template <int NB, bool FUSE>
 __device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
                                        const SpanIds<NB>& ids) {
   SpanRef<NB> s;
-  if (j == kSpare) {   // loads that are never used: block 0's tile, nothing stored
-    const bool arr = FUSE && it.arriving;
-    s.k_src = arr ? p.k_stage : p.k_cache;
-    s.v_src = arr ? p.v_stage : p.v_cache;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      s.ts[b] = it.g;
-      s.td[b] = -1;
-    }
-    s.t = 0;
-    s.bad = 0;
-    return s;
-  }
-  s.t = j * NB * kBlock;
+  // kSpare: loads that are never used read block 0's tile, nothing is stored
+  const bool spare = j == kSpare;
+  s.t = spare ? 0 : j * NB * kBlock;
   s.bad = 0;
   const int nb = max(1, min(NB, (it.L - s.t + kBlock - 1) / kBlock));
   const bool arr = FUSE && it.arriving;
@@ -331,7 +320,7 @@ __device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
   int32_t ts0 = 0;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    const int32_t sid = ids.src[b];
+    const int32_t sid = spare ? 0 : ids.src[b];
     const bool here = b < nb;
     const bool sbad = sid < 0 || sid >= src_blocks;
     if (here && sbad) s.bad |= 1u << b;
@@ -340,7 +329,7 @@ __device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
     s.ts[b] = (here && !sbad) ? ts : ts0;
     const int32_t did = ids.dst[b];
     const bool dbad = did < 0 || did >= p.num_blocks;
-    s.td[b] = (arr && here && !sbad && !dbad) ? did * p.num_kv_heads + it.g : -1;
+    s.td[b] = (arr && here && !sbad && !dbad && !spare) ? did * p.num_kv_heads + it.g : -1;
   }
   return s;
 }
