@@ -739,6 +739,21 @@ struct Ranges {
   }
 };
 
+// Waves a launch of W waves uses for a batch of T spans of NB blocks: about
+// one per kBlocksPerWave blocks (a multiple of 4, at least kMinWaves), at most
+// W.  A small batch spread over every resident wave cuts each item into
+// one-span parts whose merge costs more than the streaming (a one-request
+// round ran in 65 us on 1024 waves and 29 us on 64).  Every kernel derives
+// the same count from T.
+constexpr int kBlocksPerWave = 20;
+constexpr int kMinWaves = 64;
+
+template <int NB>
+__device__ inline int64_t waves_for(int64_t T, int64_t W) {
+  const int64_t want = (T * NB + kBlocksPerWave - 1) / kBlocksPerWave;
+  return min(W, max((int64_t)kMinWaves, (want + 3) / 4 * 4));
+}
+
 // Work-order position whose spans [hkv*pre[i], hkv*pre[i+1]) contain span s.
 __device__ inline int find_position(const uint32_t* pre, int bs, int hkv, int64_t s) {
   int lo = 0, hi = bs - 1;
@@ -962,8 +977,10 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
 
   const int64_t hkv = p.num_kv_heads;
   const int64_t ta = hkv * s_pre[n_res], tb = hkv * s_pre[p.bs] - ta;
-  const Ranges ra(ta, p.num_waves, p.w_even, p.w_odd), rb(tb, p.num_waves, p.w_even, p.w_odd_b);
+  const int64_t W = waves_for<NB>(ta + tb, p.num_waves);
   const int64_t rid = (int64_t)blockIdx.x * 4 + wave;
+  if (rid >= W) return;   // a batch too small for every resident wave
+  const Ranges ra(ta, W, p.w_even, p.w_odd), rb(tb, W, p.w_even, p.w_odd_b);
   // this wave's output buffer follows the span prefix and the work order
   OutBuf ob;
   ob.base = (char*)s_pre + p.out_off + wave * p.out_cap;
@@ -1003,7 +1020,8 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const bool seg_b = pos >= n_res;
   const int64_t off = seg_b ? ta : 0;
   const int64_t qoff = seg_b ? p.num_waves : 0;
-  const Ranges R(seg_b ? (int64_t)hkv * p.prefix[p.bs] - ta : ta, p.num_waves, p.w_even,
+  const int64_t W = waves_for<NB>((int64_t)hkv * p.prefix[p.bs], p.num_waves);
+  const Ranges R(seg_b ? (int64_t)hkv * p.prefix[p.bs] - ta : ta, W, p.w_even,
                  seg_b ? p.w_odd_b : p.w_odd);
   const int L = clamp_len(p, p.seq_lens, r);
   const int n = spans_of<NB>(L);
