@@ -38,8 +38,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--ceiling", action="store_true",
                     help="only the HBM probe: the fused pass's read/write mix on verify_8b with "
-                         "the written tiles placed three ways (gathered at the end of every "
-                         "wave's sequence, spread through it, or on a share of the waves)")
+                         "the written tiles placed four ways (gathered at the end of every "
+                         "wave's sequence, spread through it, on a share of the waves, or "
+                         "stored by waves that do not read), and the writes alone")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the practical-ceiling probe of the dominant kernel's access pattern")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -899,7 +900,7 @@ def sweep_bench(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; use --gpus 1"}))
+        print(json.dumps({"error": "the verification round runs on one GPU: the library has no multi-GPU path; use --gpus 1"}))
         sys.exit(2)
     if args.schedule:
         schedule_bench(args)

@@ -7,7 +7,7 @@
 // preparation pass also writes the tiles of arriving requests back to other
 // random positions.  nsd_probe_tiles reproduces exactly that traffic without
 // any arithmetic, so its rate is what the memory system gives this pattern,
-// against which the real kernels are judged (beside the 8 TB/s peak).
+// the rate the real kernels are measured against (beside the 8 TB/s peak).
 //
 // Separate library (libnsd_probe.so): measurement only, not part of the round.
 #include <hip/hip_runtime.h>
