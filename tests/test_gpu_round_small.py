@@ -135,6 +135,23 @@ def test_ragged_batch_of_64(device):
         _check_all(cfg, meta, device, waves=36, fused=fused)
 
 
+@pytest.mark.parametrize("bs", [1, 4, 12])
+def test_small_batches_of_long_requests(device, bs):
+    """Small batches of verify_8b-shaped requests (32/8 heads, head_dim 128,
+    contexts up to 4096, K = 4): the launch uses only about one wave per 20
+    K/V blocks, and every item is cut into parts that the merge kernel
+    combines.  Every request is checked, fused and not."""
+    rng = np.random.default_rng(40 + bs)
+    lens = rng.integers(1024, 4097, bs)
+    depth = np.full(bs, 4)
+    cfg = custom_config(seed=41 + bs, bs=bs, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                        vocab=4096, n_arriving=max(1, bs // 3), pool_blocks=None, k_lo=4,
+                        k_hi=4)
+    meta = make_meta(cfg, seq_lens=lens, depth=depth)
+    for fused in (False, True):
+        _check_all(cfg, meta, device, fused=fused)
+
+
 @pytest.mark.parametrize("fused", [False, True])
 def test_largest_batch(device, fused):
     """The largest batch the attention entry points take (8192 requests): the
