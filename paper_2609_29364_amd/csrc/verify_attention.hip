@@ -739,18 +739,23 @@ struct Ranges {
   }
 };
 
-// Waves a launch of W waves uses for a batch of T spans of NB blocks: about
-// one per kBlocksPerWave blocks (a multiple of 4, at least kMinWaves), at most
-// W.  A small batch spread over every resident wave cuts each item into
-// one-span parts whose merge costs more than the streaming (a one-request
-// round ran in 65 us on 1024 waves and 29 us on 64).  Every kernel derives
-// the same count from T.
-constexpr int kBlocksPerWave = 20;
+// Waves a launch of W waves uses for a batch of T spans of NB blocks (B = T
+// NB blocks), a multiple of 4, at least kMinWaves, at most W.  A small batch
+// spread over every resident wave cuts each item into one-span parts whose
+// merge costs more than the streaming (a one-request round ran in 65 us on
+// 1024 waves and 29 us on 64); too few waves leave HBM idle.  Measured on
+// MI355X: the separate attention (four-block spans) is best at about one
+// wave per 20 blocks; the fused pass at B / (15 + B / 1000) waves (about 15
+// blocks per wave at 1k blocks, 30 at 10-20k, 80 at 60k), and with every
+// resident wave once that passes 7/8 of them.  Every kernel derives the
+// same count from T.
 constexpr int kMinWaves = 64;
 
-template <int NB>
+template <int NB, bool FUSE>
 __device__ inline int64_t waves_for(int64_t T, int64_t W) {
-  const int64_t want = (T * NB + kBlocksPerWave - 1) / kBlocksPerWave;
+  const int64_t B = T * NB;
+  int64_t want = FUSE ? B * 1000 / (15000 + B) : (B + 19) / 20;
+  if (FUSE && 8 * want > 7 * W) want = W;
   return min(W, max((int64_t)kMinWaves, (want + 3) / 4 * 4));
 }
 
@@ -977,7 +982,7 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
 
   const int64_t hkv = p.num_kv_heads;
   const int64_t ta = hkv * s_pre[n_res], tb = hkv * s_pre[p.bs] - ta;
-  const int64_t W = waves_for<NB>(ta + tb, p.num_waves);
+  const int64_t W = waves_for<NB, FUSE>(ta + tb, p.num_waves);
   const int64_t rid = (int64_t)blockIdx.x * 4 + wave;
   if (rid >= W) return;   // a batch too small for every resident wave
   const Ranges ra(ta, W, p.w_even, p.w_odd), rb(tb, W, p.w_even, p.w_odd_b);
@@ -1005,8 +1010,9 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
 // (deterministic, no atomics).  One workgroup per (KV head, request); the
 // ranges holding the item's spans and their partial slots are found once per
 // workgroup.
-template <int D, int MT, int NB>
+template <int D, int MT, bool FUSE>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
+  constexpr int NB = span_blocks(D, MT, FUSE);
   __shared__ int64_t s_slot[256];   // partial slots of the item, in range order
   __shared__ int s_nslot;
   const int g = blockIdx.x;
@@ -1020,7 +1026,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const bool seg_b = pos >= n_res;
   const int64_t off = seg_b ? ta : 0;
   const int64_t qoff = seg_b ? p.num_waves : 0;
-  const int64_t W = waves_for<NB>((int64_t)hkv * p.prefix[p.bs], p.num_waves);
+  const int64_t W = waves_for<NB, FUSE>((int64_t)hkv * p.prefix[p.bs], p.num_waves);
   const Ranges R(seg_b ? (int64_t)hkv * p.prefix[p.bs] - ta : ta, W, p.w_even,
                  seg_b ? p.w_odd_b : p.w_odd);
   const int L = clamp_len(p, p.seq_lens, r);
@@ -1187,7 +1193,7 @@ void launch(const Params& p, int bs, size_t lds_bytes, hipStream_t stream) {
   hipLaunchKernelGGL((verify_attention_kernel<D, MT, FUSE>), dim3(p.num_waves / 4), dim3(256),
                      lds_bytes, stream, p, p.block_table, p.stage_table, p.seq_lens,
                      p.q_indptr);
-  hipLaunchKernelGGL((combine_kernel<D, MT, span_blocks(D, MT, FUSE)>), dim3(p.num_kv_heads, bs),
+  hipLaunchKernelGGL((combine_kernel<D, MT, FUSE>), dim3(p.num_kv_heads, bs),
                      dim3(256), 0, stream, p);
 }
 
