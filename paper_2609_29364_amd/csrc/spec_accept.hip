@@ -5,7 +5,10 @@
 //
 // A request's weight row (max(0, p_n - q_n) after a rejection at n, or the
 // bonus row p_K) is 151936 floats in the workloads: streaming it is the whole
-// cost.  Two kernels:
+// cost.  A batch with a row for every CU runs accept_row_kernel: one
+// 1024-thread workgroup per row takes the acceptance tests, streams the row
+// into chunk sums held in LDS, and draws, in one launch.  A smaller batch
+// spreads each row over several workgroups, in two kernels:
 //
 // 1. row_sums_kernel, one 256-thread workgroup per (row, segment of 64
 //    chunks).  Every workgroup first evaluates the request's K acceptance
@@ -34,6 +37,7 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 256;       // weights per chunk: 64 lanes x 4
 constexpr int kUnroll = 4;
+constexpr int kRowThreads = 1024;   // accept_row_kernel: 16 waves per row
 constexpr int kSegChunks = kWaves * kUnroll * 4;   // chunks per row_sums workgroup
 constexpr int kMaxVocab = 1 << 19;
 constexpr int kMaxChunks = kMaxVocab / kChunk;
@@ -114,14 +118,16 @@ __device__ inline const float* row_p(const Args& A, int r, int a, int n) {
   return SAMPLE ? A.p + (int64_t)r * A.row_stride : A.p + (int64_t)(a + n) * A.vocab;
 }
 
-// Sums of chunks [c_beg, c_end) of the weight row into dst[c].
+// Sums of chunks [c_beg, c_end) of the weight row into dst[c], by the NW
+// waves of a workgroup.
+template <int NW>
 __device__ inline void chunk_sums(const float* prow, const float* qrow, bool resid, int vocab,
                                   int c_beg, int c_end, int lane, int wave, double* dst) {
-  for (int c0 = c_beg + wave; c0 < c_end; c0 += kWaves * kUnroll) {
+  for (int c0 = c_beg + wave; c0 < c_end; c0 += NW * kUnroll) {
     f32x4 pv[kUnroll], qv[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int c = c0 + u * kWaves;
+      const int c = c0 + u * NW;
       const int idx = c * kChunk + lane * 4;
       pv[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
       qv[u] = pv[u];
@@ -147,7 +153,7 @@ __device__ inline void chunk_sums(const float* prow, const float* qrow, bool res
 #pragma unroll
     for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o);
     if ((lane & 15) == 0) {
-      const int c = c0 + ((h5 ? 2 : 0) + (h4 ? 1 : 0)) * kWaves;
+      const int c = c0 + ((h5 ? 2 : 0) + (h4 ? 1 : 0)) * NW;
       if (c < c_end) dst[c] = s;
     }
   }
@@ -174,12 +180,14 @@ __global__ __launch_bounds__(kThreads) void row_sums_kernel(Args A) {
   const float* qrow = resid ? A.q + (int64_t)(a - r + n) * A.vocab : prow;
   const int c_beg = seg * kSegChunks;
   const int c_end = min(A.nchunk, c_beg + kSegChunks);
-  chunk_sums(prow, qrow, resid, A.vocab, c_beg, c_end, lane, wave,
-             A.ws_sum + (int64_t)r * A.nchunk);
+  chunk_sums<kWaves>(prow, qrow, resid, A.vocab, c_beg, c_end, lane, wave,
+                     A.ws_sum + (int64_t)r * A.nchunk);
   if (!SAMPLE && seg == 0 && threadIdx.x == 0) A.ws_n[r] = n;
 }
 
-// Exclusive block scan of one value per thread; *total gets the block's sum.
+// Exclusive scan of one value per thread over the NW waves of a workgroup;
+// *total gets the workgroup's sum.
+template <int NW>
 __device__ inline double block_excl_scan(double v, int lane, int wave, double* s_w,
                                          double* total) {
   const double incl = wave_incl_scan(v, lane);
@@ -189,7 +197,7 @@ __device__ inline double block_excl_scan(double v, int lane, int wave, double* s
   __syncthreads();
   double off = 0.0, all = 0.0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < NW; ++w) {
     if (w < wave) off += s_w[w];
     all += s_w[w];
   }
@@ -198,43 +206,34 @@ __device__ inline double block_excl_scan(double v, int lane, int wave, double* s
   return off + excl;
 }
 
-template <bool SAMPLE>
-__global__ __launch_bounds__(kThreads) void pick_kernel(Args A) {
-  __shared__ double s_sum[kMaxChunks];
-  __shared__ double s_w[kWaves];
-  __shared__ double s_pre;
-  __shared__ int s_c;
+// The draw of request r (or sample row r) from its chunk sums s_sum[0,
+// nchunk), by a workgroup of NT threads: thread tid owns consecutive chunks,
+// a block scan of the thread totals finds the first chunk whose inclusive
+// prefix exceeds tau = u_K * S, and wave 0 scans inside that chunk.  Writes
+// the request's tokens and accepted length.
+template <bool SAMPLE, int NT>
+__device__ inline void pick_row(const Args& A, int r, int a, int k, int n, double* s_sum,
+                                double* s_w, double& s_pre, int& s_c) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int r = blockIdx.x;
   const int nchunk = A.nchunk;
-  int a = r, k = 0, n = 0;
-  if (!SAMPLE) {
-    a = A.q_indptr[r];
-    k = max(0, min(A.q_indptr[r + 1] - a - 1, A.max_k));
-    n = min(max(A.ws_n[r], 0), k);
-  }
   bool resid = n < k;
   const float* prow = row_p<SAMPLE>(A, r, a, n);
   const float* qrow = resid ? A.q + (int64_t)(a - r + n) * A.vocab : prow;
-  const double* sums = A.ws_sum + (int64_t)r * nchunk;
-  for (int c = tid; c < nchunk; c += kThreads) s_sum[c] = sums[c];
-  __syncthreads();
-
   // thread tid owns chunks [c0, c1)
-  const int per = (nchunk + kThreads - 1) / kThreads;
+  const int per = (nchunk + NT - 1) / NT;
   const int c0 = min(nchunk, tid * per), c1 = min(nchunk, c0 + per);
   double total = 0.0, pre = 0.0;
   for (int attempt = 0; attempt < 2; ++attempt) {
     double local = 0.0;
     for (int c = c0; c < c1; ++c) local += s_sum[c];
-    pre = block_excl_scan(local, lane, wave, s_w, &total);
+    pre = block_excl_scan<NT / 64>(local, lane, wave, s_w, &total);
     if (total > 0.0 || !resid) break;
     // residual without mass: draw from p_n itself
     resid = false;
     qrow = prow;
-    chunk_sums(prow, qrow, false, A.vocab, 0, nchunk, lane, wave, s_sum);
+    chunk_sums<NT / 64>(prow, qrow, false, A.vocab, 0, nchunk, lane, wave, s_sum);
     __syncthreads();
   }
   const double tau = (double)A.u[a + k] * total;
@@ -327,6 +326,55 @@ __global__ __launch_bounds__(kThreads) void pick_kernel(Args A) {
   if (lane == 0) A.accepted_len[r] = n;
 }
 
+template <bool SAMPLE>
+__global__ __launch_bounds__(kThreads) void pick_kernel(Args A) {
+  __shared__ double s_sum[kMaxChunks];
+  __shared__ double s_w[kWaves];
+  __shared__ double s_pre;
+  __shared__ int s_c;
+  const int tid = threadIdx.x;
+  const int r = blockIdx.x;
+  int a = r, k = 0, n = 0;
+  if (!SAMPLE) {
+    a = A.q_indptr[r];
+    k = max(0, min(A.q_indptr[r + 1] - a - 1, A.max_k));
+    n = min(max(A.ws_n[r], 0), k);
+  }
+  const double* sums = A.ws_sum + (int64_t)r * A.nchunk;
+  for (int c = tid; c < A.nchunk; c += kThreads) s_sum[c] = sums[c];
+  __syncthreads();
+  pick_row<SAMPLE, kThreads>(A, r, a, k, n, s_sum, s_w, s_pre, s_c);
+}
+
+// Both steps for one row per workgroup of kRowThreads threads (used when the
+// batch has at least a row per CU): the acceptance tests, the row's chunk
+// sums into LDS, then the draw, with no second launch and no round trip of
+// the sums through memory.
+template <bool SAMPLE>
+__global__ __launch_bounds__(kRowThreads) void accept_row_kernel(Args A) {
+  __shared__ double s_sum[kMaxChunks];
+  __shared__ double s_w[kRowThreads / 64];
+  __shared__ double s_pre;
+  __shared__ int s_c;
+  __shared__ int s_n;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r = blockIdx.x;
+  int a, k;
+  acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n);
+  int n = 0;
+  if (!SAMPLE) {
+    __syncthreads();
+    n = s_n;
+  }
+  const bool resid = n < k;
+  const float* prow = row_p<SAMPLE>(A, r, a, n);
+  const float* qrow = resid ? A.q + (int64_t)(a - r + n) * A.vocab : prow;
+  chunk_sums<kRowThreads / 64>(prow, qrow, resid, A.vocab, 0, A.nchunk, lane, wave, s_sum);
+  __syncthreads();
+  pick_row<SAMPLE, kRowThreads>(A, r, a, k, n, s_sum, s_w, s_pre, s_c);
+}
+
 int64_t sums_bytes(int64_t rows, int32_t vocab) {
   const int64_t nchunk = (vocab + kChunk - 1) / kChunk;
   return (rows * nchunk * 8 + 255) / 256 * 256;
@@ -345,8 +393,24 @@ nsd_status launch(bool sample, Args A, int32_t rows, void* workspace, size_t wor
   A.ws_sum = (double*)workspace;
   A.ws_n = (int32_t*)((char*)workspace + sums_bytes(rows, A.vocab));
   const dim3 g1((uint32_t)((A.nchunk + kSegChunks - 1) / kSegChunks) * (uint32_t)rows);
+  // a batch with a row for every CU: one workgroup per row does both steps;
+  // a smaller one spreads every row over several workgroups
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    cus = 256;
+  }
+  const bool one_pass = rows >= cus;
   clear_stale_error();
-  if (sample) {
+  if (one_pass) {
+    if (sample)
+      hipLaunchKernelGGL(accept_row_kernel<true>, dim3(rows), dim3(kRowThreads), 0,
+                         (hipStream_t)stream, A);
+    else
+      hipLaunchKernelGGL(accept_row_kernel<false>, dim3(rows), dim3(kRowThreads), 0,
+                         (hipStream_t)stream, A);
+  } else if (sample) {
     hipLaunchKernelGGL(row_sums_kernel<true>, g1, dim3(kThreads), 0, (hipStream_t)stream, A);
     hipLaunchKernelGGL(pick_kernel<true>, dim3(rows), dim3(kThreads), 0, (hipStream_t)stream, A);
   } else {
