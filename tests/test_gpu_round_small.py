@@ -390,7 +390,9 @@ def test_accept_identical_rows_accept_all(device):
     check_accept(p, q, x, u, q_indptr, acc, tok)
 
 
-def test_accept_special_cases(device):
+def _special_cases():
+    """Five requests: forced one-hot residual, out-of-vocabulary proposal with
+    an empty residual, exact tie, K = 0 at u = 1 - 2^-24, u on a CDF boundary."""
     vocab = 16
     depth = [1, 1, 1, 0, 2]
     q_indptr, tq, bs = _batch(depth)
@@ -426,13 +428,38 @@ def test_accept_special_cases(device):
     x[3], x[4] = 0, 1
     p[a + 2] = np.array([0.25, 0.25, 0, 0.5] + [0] * 12, np.float32)
     u[a + 2] = 0.25
+    return p, q, x, u, depth
+
+
+def _check_special(acc, tok, q_indptr, r0=0):
+    assert list(acc[r0:r0 + 5]) == [0, 0, 1, 0, 2]
+    assert tok[q_indptr[r0]] == 9
+    assert tok[q_indptr[r0 + 2]:q_indptr[r0 + 2] + 2].tolist() == [7, 12]
+    assert tok[q_indptr[r0 + 3]] == 5
+    assert tok[q_indptr[r0 + 4] + 2] == 1
+
+
+def test_accept_special_cases(device):
+    p, q, x, u, depth = _special_cases()
+    q_indptr, _, _ = _batch(depth)
     acc, tok = _accept(device, p, q, x, u, q_indptr, 2)
-    assert list(acc) == [0, 0, 1, 0, 2]
-    assert tok[q_indptr[0]] == 9
-    assert tok[q_indptr[2]:q_indptr[2] + 2].tolist() == [7, 12]
-    assert tok[q_indptr[3]] == 5
-    assert tok[q_indptr[4] + 2] == 1
+    _check_special(acc, tok, q_indptr)
     check_accept(p, q, x, u, q_indptr, acc, tok)
+
+
+def test_accept_special_cases_one_pass(device):
+    """The same cases in a batch with more rows than the device has CUs, which
+    takes the one-kernel path (one workgroup per row, sums kept in LDS)."""
+    p, q, x, u, depth = _special_cases()
+    reps = 60
+    assert reps * len(depth) >= torch.cuda.get_device_properties(device).multi_processor_count
+    q_indptr, _, _ = _batch(depth * reps)
+    pt, qt = np.tile(p, (reps, 1)), np.tile(q, (reps, 1))
+    xt, ut = np.tile(x, reps), np.tile(u, reps)
+    acc, tok = _accept(device, pt, qt, xt, ut, q_indptr, 2)
+    for rep in range(reps):
+        _check_special(acc, tok, q_indptr, rep * len(depth))
+    check_accept(pt, qt, xt, ut, q_indptr, acc, tok)
 
 
 def test_accept_workspace_contents_do_not_matter(device):
