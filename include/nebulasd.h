@@ -22,14 +22,21 @@
  *   `stream` can read/write; all work is enqueued on `stream` (a hipStream_t,
  *   NULL = the null stream) and the call returns without waiting.  The caller
  *   owns every buffer, including workspaces, and keeps it alive until the
- *   stream has passed the call.  The library allocates nothing and keeps no
- *   state besides a thread-local error message.
+ *   stream has passed the call.  The library allocates nothing.  Its state
+ *   is a thread-local error message, launch facts it queries once per device
+ *   (CU count, occupancy, LDS size) and the wave count of
+ *   nsd_set_attention_waves.
  * - Arguments are validated on the host before anything is enqueued; a bad
  *   scalar or NULL pointer returns an error status and enqueues nothing.
  *   Device-resident contents (block ids, lengths, offsets, tokens) are not
  *   visible to the host: contents outside the documented ranges give
  *   unspecified results, but every kernel clamps them so that it never reads
- *   or writes outside the buffers whose sizes the scalars describe.
+ *   or writes outside the buffers whose sizes the scalars describe.  The one
+ *   device-resident size is the row count total_q = q_indptr[bs] of the
+ *   query-row buffers (q, out, target rows, uniforms, window rows), which
+ *   must equal their rows; every other q_indptr entry is clamped into
+ *   [0, total_q].  nsd_check_plan / nsd_check_pairs validate host copies of
+ *   the metadata against the documented ranges before a round runs.
  * - Calls never abort and never print.  Calls on different streams with
  *   disjoint outputs may run concurrently.
  * - bf16 is bfloat16 (1 sign, 8 exponent, 7 mantissa bits) stored in 2 bytes.
@@ -107,15 +114,27 @@ nsd_status nsd_kv_gather(const void* src_k, const void* src_v, int64_t src_num_b
 
 /*
  * Bytes of workspace nsd_verify_attention and nsd_gather_verify_attention
- * need for these sizes on the
- * current HIP device (0 if the sizes are invalid).  The size depends on the
- * arguments and on how many waves the device keeps resident (its CU count);
- * the environment variable NSD_ATTN_WAVES (a positive multiple of 4), if set,
- * overrides that wave count for both this query and the launch.
+ * need for these sizes on the current HIP device (0 if the sizes are
+ * invalid).  The size depends on the arguments and on how many waves the
+ * device keeps resident (its CU count), or on the count set with
+ * nsd_set_attention_waves.
  */
 size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
                                            int32_t num_kv_heads, int32_t head_dim,
                                            int32_t max_q_per_seq, int32_t max_seq_len);
+
+/*
+ * Test and tuning hook: the attention entry points and the workspace query
+ * split their work over `waves` resident waves (a positive multiple of 4, at
+ * most 2^20) instead of the device's own count; 0 restores the device's
+ * count.  Process-wide: set it only while no other thread queries workspace
+ * sizes or launches attention.  Any other value returns NSD_ERR_SHAPE.
+ * nsd_attention_waves returns the current setting (0: the device's count).
+ * Results do not depend on the wave count beyond floating-point summation
+ * order; the tests use it to force items cut into partials or whole.
+ */
+nsd_status nsd_set_attention_waves(int32_t waves);
+int32_t    nsd_attention_waves(void);
 
 /*
  * Verification attention for one layer.
@@ -141,7 +160,9 @@ size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
  *               num_blocks * num_kv_heads must not exceed 2^31 - 1.
  * seq_lens : device, int32 [bs], 1 <= L_r <= max_seq_len, L_r <= 16*max_blocks_per_seq.
  * q_indptr : device, int32 [bs+1], non-decreasing, q_indptr[0] = 0,
- *            1 <= n_q <= min(max_q_per_seq, L_r).
+ *            1 <= n_q <= min(max_q_per_seq, L_r); q_indptr[bs] = total_q must
+ *            be the row count of q and out (other entries are clamped into
+ *            [0, total_q], n_q to max_q_per_seq).
  * num_q_heads % num_kv_heads == 0; (num_q_heads/num_kv_heads) * max_q_per_seq <= 64.
  * head_dim in {64, 128}; block_size == 16.
  * scale : the softmax scale (usually 1/sqrt(head_dim)), finite.
@@ -298,7 +319,12 @@ nsd_status nsd_host_alias(const void* host, void** device_alias);
  *
  * p_target : device, fp32 [total_q][vocab];  q_draft : device, fp32 [total_q-bs][vocab]
  * draft_tokens : device, int32 [total_q-bs];  uniforms : device, fp32 [total_q], in [0,1)
- * q_indptr : device, int32 [bs+1], q_indptr[0] = 0, 0 <= K_r <= max_k.
+ * q_indptr : device, int32 [bs+1], q_indptr[0] = 0, 0 <= K_r <= max_k;
+ *            q_indptr[bs] = total_q must be the row count of p_target and
+ *            uniforms.  Other entries are clamped so that a request's target
+ *            rows stay below total_q and its draft rows inside [0, total_q-bs);
+ *            a request whose first row clamps to total_q gets accepted_len 0
+ *            and no token.
  * vocab : 4 <= vocab <= 2^19, vocab % 4 == 0; 0 <= max_k <= 63.
  * accepted_len : device, int32 [bs];  out_tokens : device, int32 [total_q].
  * Row bases must be 16-byte aligned (true for hipMalloc'd/torch tensors).
@@ -342,6 +368,42 @@ nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
 nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* uniforms,
                       int32_t n_rows, int32_t vocab, int32_t* out_tokens, int32_t out_stride,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Host validation of a round's metadata: host copies of the arrays the
+ * attention, fused and append calls read from device memory, checked against
+ * the ranges those calls document (host code; no GPU involved).
+ *
+ * Passage: Section 3 (paged blocks and a block map per request), Section 5
+ * (each request's valid length), Appendix G.2/H (anchor plus proposals per
+ * request), Appendix F.2 (capacity checks before a batch runs: block ids
+ * inside the bank, lengths inside its token limit).
+ *
+ * Checks: q_indptr[0] = 0 and, if total_q >= 0, q_indptr[bs] = total_q;
+ * every request has 1 <= L_r <= min(max_seq_len, 16 * max_blocks_per_seq)
+ * and 1 <= n_q <= min(max_q_per_seq, L_r) (so q_indptr increases); its
+ * block ids b < ceil(L_r / 16) lie in [0, num_blocks).  With a stage_table
+ * (the fused call), pool blocks are distinct over the batch, and every
+ * arriving request (entry 0 >= 0) has staging ids in [0, stage_num_blocks),
+ * distinct over the batch.  Returns NSD_OK, or NSD_ERR_SHAPE with
+ * nsd_last_error naming the first violation (NSD_ERR_NULL for a missing
+ * array).  All pointers are host memory; stage_table may be NULL.
+ */
+nsd_status nsd_check_plan(const int32_t* block_table, const int32_t* stage_table,
+                          int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                          const int32_t* q_indptr, int32_t bs, int64_t num_blocks,
+                          int64_t stage_num_blocks, int32_t max_q_per_seq, int32_t max_seq_len,
+                          int64_t total_q);
+
+/*
+ * Host validation of a gather plan (nsd_kv_gather's pairs): every source id
+ * in [0, src_num_blocks), every destination id in [0, dst_num_blocks) and
+ * destination ids distinct.  Passage: Appendix E.4 (copy plans as numeric
+ * descriptors), Appendix F.2 (block capacity).  Host pointers; returns as
+ * nsd_check_plan.
+ */
+nsd_status nsd_check_pairs(const int32_t* src_ids, const int32_t* dst_ids, int64_t n_pairs,
+                           int64_t src_num_blocks, int64_t dst_num_blocks);
 
 /*
  * Worker-triggered batch reconstruction: one scheduling opportunity (host

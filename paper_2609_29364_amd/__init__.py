@@ -51,6 +51,10 @@ _SIGS = {
                              _P]),
     "nsd_commit_lengths": (_I32, [_P, _P, _P, _P, _I32, _P]),
     "nsd_host_alias": (_I32, [_P, ctypes.POINTER(ctypes.c_void_p)]),
+    "nsd_set_attention_waves": (_I32, [_I32]),
+    "nsd_attention_waves": (_I32, []),
+    "nsd_check_plan": (_I32, [_P, _P, _I32, _P, _P, _I32, _I64, _I64, _I32, _I32, _I64]),
+    "nsd_check_pairs": (_I32, [_P, _P, _I64, _I64, _I64]),
 }
 
 
@@ -96,6 +100,67 @@ def version():
     return (v >> 16, v & 0xFFFF)
 
 
+class attention_waves:
+    """Context manager: attention calls (and workspace queries) inside it split
+    their work over ``waves`` resident waves (a positive multiple of 4) instead
+    of the device's count; ``None`` or 0 keeps the device's count.  The setting
+    is process-wide (a test and tuning hook)."""
+
+    def __init__(self, waves):
+        self.waves = int(waves or 0)
+
+    def __enter__(self):
+        self.old = lib().nsd_attention_waves()
+        _check("set_attention_waves", lib().nsd_set_attention_waves(self.waves))
+        return self
+
+    def __exit__(self, *exc):
+        _check("set_attention_waves", lib().nsd_set_attention_waves(self.old))
+        return False
+
+
+def _host_i32(a, name):
+    import numpy as np
+    if a is None:
+        return None
+    if isinstance(a, torch.Tensor):
+        a = a.cpu().numpy()
+    arr = np.ascontiguousarray(a, dtype=np.int32)
+    return arr
+
+
+def check_plan(block_table, seq_lens, q_indptr, num_blocks, max_q_per_seq, max_seq_len,
+               stage_table=None, stage_num_blocks=0, total_q=-1):
+    """Validate a round's metadata on the host (nsd_check_plan); raises NsdError
+    naming the first violation.  Arrays may be numpy arrays or tensors (copied
+    to the host)."""
+    bt = _host_i32(block_table, "block_table")
+    st = _host_i32(stage_table, "stage_table")
+    sl = _host_i32(seq_lens, "seq_lens")
+    qi = _host_i32(q_indptr, "q_indptr")
+    bs = len(sl)
+    if bt.ndim != 2 or bt.shape[0] != bs or len(qi) != bs + 1 or \
+            (st is not None and st.shape != bt.shape):
+        raise ValueError("block_table / stage_table / q_indptr do not match seq_lens")
+    _check("check_plan", lib().nsd_check_plan(
+        bt.ctypes.data if bs else None, st.ctypes.data if st is not None and bs else None,
+        max(1, bt.shape[1]), sl.ctypes.data if bs else None, qi.ctypes.data, bs,
+        int(num_blocks), int(stage_num_blocks), int(max_q_per_seq), int(max_seq_len),
+        int(total_q)))
+
+
+def check_pairs(src_ids, dst_ids, src_num_blocks, dst_num_blocks):
+    """Validate a gather plan on the host (nsd_check_pairs); raises NsdError."""
+    s = _host_i32(src_ids, "src_ids")
+    d = _host_i32(dst_ids, "dst_ids")
+    if s.shape != d.shape:
+        raise ValueError("src_ids and dst_ids differ in length")
+    n = len(s)
+    _check("check_pairs", lib().nsd_check_pairs(
+        s.ctypes.data if n else None, d.ctypes.data if n else None, n, int(src_num_blocks),
+        int(dst_num_blocks)))
+
+
 def kv_gather(src_k, src_v, dst_k, dst_v, src_ids, dst_ids, layer0=0, n_layers=None):
     """Copy whole KV blocks src -> dst for every pair and layer (in place on dst).
 
@@ -137,6 +202,17 @@ def new_workspace(nbytes, device):
     return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 
 
+def _attn_ws(workspace, need, q):
+    """The caller's workspace (checked) or a new one of `need` bytes; (tensor, bytes)."""
+    if workspace is None:
+        workspace = new_workspace(need, q.device) if need else None
+    else:
+        _dev(workspace, torch.uint8, "workspace")
+        if workspace.device != q.device:
+            raise ValueError("workspace must be on q's device")
+    return workspace, (0 if workspace is None else workspace.numel())
+
+
 def verify_attention(q, k_cache, v_cache, block_table, seq_lens, q_indptr, max_q_per_seq,
                      max_seq_len, scale=None, out=None, workspace=None):
     """One layer of verification attention; returns out [total_q][Hq][D] bf16.
@@ -166,9 +242,7 @@ def verify_attention(q, k_cache, v_cache, block_table, seq_lens, q_indptr, max_q
         if out.shape != q.shape:
             raise ValueError("out must have q's shape")
     need = verify_attention_workspace_size(bs, hq, hkv, d, max_q_per_seq, max_seq_len)
-    if workspace is None and need:
-        workspace = new_workspace(need, q.device)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    workspace, ws_bytes = _attn_ws(workspace, need, q)
     _check("verify_attention", lib().nsd_verify_attention(
         _ptr(q), _ptr(k_cache), _ptr(v_cache), nb, _ptr(block_table), block_table.shape[1],
         _ptr(seq_lens), _ptr(q_indptr), bs, hq, hkv, d, bsz, max_q_per_seq, max_seq_len,
@@ -206,12 +280,12 @@ def gather_verify_attention(q, k_cache, v_cache, k_stage, v_stage, block_table, 
         scale = 1.0 / math.sqrt(d)
     if out is None:
         out = torch.empty_like(q)
-    elif out.shape != q.shape:
-        raise ValueError("out must have q's shape")
+    else:
+        _dev(out, torch.bfloat16, "out")
+        if out.shape != q.shape:
+            raise ValueError("out must have q's shape")
     need = verify_attention_workspace_size(bs, hq, hkv, d, max_q_per_seq, max_seq_len)
-    if workspace is None and need:
-        workspace = new_workspace(need, q.device)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    workspace, ws_bytes = _attn_ws(workspace, need, q)
     _check("gather_verify_attention", lib().nsd_gather_verify_attention(
         _ptr(q), _ptr(k_cache), _ptr(v_cache), nb, _ptr(k_stage), _ptr(v_stage),
         k_stage.shape[0], _ptr(block_table), _ptr(stage_table), block_table.shape[1],
@@ -229,9 +303,10 @@ def _accept_ws(workspace, rows, vocab, device):
     need = accept_workspace_size(rows, vocab)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
-    if not workspace.is_cuda or not workspace.is_contiguous():
-        raise ValueError("workspace must be a contiguous GPU tensor")
-    return workspace, workspace.numel() * workspace.element_size()
+    _dev(workspace, torch.uint8, "workspace")
+    if workspace.device != device:
+        raise ValueError("workspace must be on the probabilities' device")
+    return workspace, workspace.numel()
 
 
 def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, accepted_len=None,
@@ -372,7 +447,7 @@ def kv_writeback(k_pool, v_pool, host_k, host_v, src_ids, dst_ids):
         BLOCK_SIZE, d, _stream(k_pool)))
 
 
-__all__ = ["lib", "version", "kv_gather", "verify_attention", "verify_attention_workspace_size",
+__all__ = ["lib", "version", "attention_waves", "check_plan", "check_pairs", "kv_gather", "verify_attention", "verify_attention_workspace_size",
            "new_workspace", "gather_verify_attention", "copy_plan", "COPY_H2D", "COPY_D2H",
            "DEFAULT_CHUNK", "kv_append", "commit_lengths", "host_alias", "kv_writeback",
            "spec_accept", "accept_workspace_size", "sample", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

@@ -10,7 +10,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(HERE, "libnebulasd.so")
 SOURCES = ["status.cpp", "kv_gather.hip", "verify_attention.hip", "spec_accept.hip",
-           "copy_plan.cpp", "kv_commit.hip", "scheduler.cpp"]
+           "copy_plan.cpp", "kv_commit.hip", "scheduler.cpp", "check_plan.cpp"]
 # bandwidth probes for the measurement of practical ceilings: a library of their own
 PROBE_SOURCES = ["hbm_probe.hip"]
 PROBE_LIB_PATH = os.path.join(HERE, "libnsd_probe.so")

@@ -51,6 +51,7 @@ struct Args {
   const int32_t* x;            // proposal tokens
   const float* u;              // uniforms
   const int32_t* q_indptr;     // [rows + 1] (not SAMPLE)
+  int32_t rows;                // requests (not SAMPLE) or sample rows
   int32_t vocab, max_k, nchunk;
   int64_t row_stride;          // SAMPLE: elements between rows
   int32_t out_stride;          // SAMPLE: entries between output tokens
@@ -84,18 +85,35 @@ __device__ inline void weights4(const f32x4& pv, const f32x4& qv, bool resid, do
   }
 }
 
+// Request r's first target row a and proposal count k, read from q_indptr
+// and clamped so that every row the request touches lies in the buffers the
+// row count total_q = q_indptr[rows] describes: target rows a .. a + k <
+// total_q, draft rows a - r .. a - r + k - 1 inside [0, total_q - rows).  For
+// a well-formed q_indptr (non-decreasing, every request at least one row)
+// nothing changes.  Returns false when the request has no target row (its
+// start clamps to total_q); it then draws nothing and writes no token.
+__device__ inline bool request_rows(const Args& A, int r, int& a, int& k) {
+  const int total = max(0, A.q_indptr[A.rows]);
+  a = min(max(A.q_indptr[r], 0), total);
+  k = max(0, min(min(A.q_indptr[r + 1] - a - 1, A.max_k), total - a - 1));
+  const int db = a - r;   // first draft row
+  if (db < 0) k = 0;
+  k = min(k, max(0, total - A.rows - db));
+  return a < total;
+}
+
 // Request r's first row a and clamped proposal count k; wave 0 evaluates the
-// acceptance tests and leaves the first rejection n in *s_n.
+// acceptance tests and leaves the first rejection n in *s_n.  Returns false
+// when the request has no row (nothing to test or draw).
 template <bool SAMPLE>
-__device__ inline void acceptance(const Args& A, int r, int lane, int wave, int& a, int& k,
+__device__ inline bool acceptance(const Args& A, int r, int lane, int wave, int& a, int& k,
                                   int* s_n) {
   if (SAMPLE) {
     a = r;
     k = 0;
-    return;
+    return true;
   }
-  a = A.q_indptr[r];
-  k = max(0, min(A.q_indptr[r + 1] - a - 1, A.max_k));
+  if (!request_rows(A, r, a, k)) return false;
   if (wave == 0) {
     bool ok = true;
     if (lane < k) {
@@ -111,6 +129,7 @@ __device__ inline void acceptance(const Args& A, int r, int lane, int wave, int&
     const uint64_t rejected = __ballot(!ok);
     if (lane == 0) *s_n = rejected ? (__ffsll((unsigned long long)rejected) - 1) : k;
   }
+  return true;
 }
 
 template <bool SAMPLE>
@@ -169,7 +188,10 @@ __global__ __launch_bounds__(kThreads) void row_sums_kernel(Args A) {
   const int r = blockIdx.x / nseg;
   const int seg = blockIdx.x - r * nseg;
   int a, k;
-  acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n);
+  if (!acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n)) {
+    if (seg == 0 && threadIdx.x == 0) A.ws_n[r] = 0;
+    return;   // uniform over the workgroup: no row to stream
+  }
   int n = 0;
   if (!SAMPLE) {
     __syncthreads();
@@ -336,8 +358,10 @@ __global__ __launch_bounds__(kThreads) void pick_kernel(Args A) {
   const int r = blockIdx.x;
   int a = r, k = 0, n = 0;
   if (!SAMPLE) {
-    a = A.q_indptr[r];
-    k = max(0, min(A.q_indptr[r + 1] - a - 1, A.max_k));
+    if (!request_rows(A, r, a, k)) {
+      if (tid == 0) A.accepted_len[r] = 0;
+      return;
+    }
     n = min(max(A.ws_n[r], 0), k);
   }
   const double* sums = A.ws_sum + (int64_t)r * A.nchunk;
@@ -361,7 +385,10 @@ __global__ __launch_bounds__(kRowThreads) void accept_row_kernel(Args A) {
   const int wave = threadIdx.x >> 6;
   const int r = blockIdx.x;
   int a, k;
-  acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n);
+  if (!acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n)) {
+    if (threadIdx.x == 0) A.accepted_len[r] = 0;
+    return;
+  }
   int n = 0;
   if (!SAMPLE) {
     __syncthreads();
@@ -447,8 +474,8 @@ extern "C" nsd_status nsd_spec_accept(const float* p_target, const float* q_draf
     return fail(NSD_ERR_NULL, "spec_accept: NULL pointer argument");
   if (((uintptr_t)p_target | (uintptr_t)(max_k > 0 ? q_draft : p_target)) & 15)
     return fail(NSD_ERR_SHAPE, "spec_accept: probability rows must be 16-byte aligned");
-  Args A{p_target, q_draft, draft_tokens, uniforms, q_indptr, vocab, max_k, 0, (int64_t)vocab, 1,
-         nullptr, nullptr, accepted_len, out_tokens};
+  Args A{p_target, q_draft, draft_tokens, uniforms, q_indptr, bs, vocab, max_k, 0,
+         (int64_t)vocab, 1, nullptr, nullptr, accepted_len, out_tokens};
   return launch(false, A, bs, workspace, workspace_bytes, stream, "spec_accept");
 }
 
@@ -469,7 +496,7 @@ extern "C" nsd_status nsd_sample(const float* probs, int64_t row_stride, const f
   if (n_rows == 0) return NSD_OK;
   if (!probs || !uniforms || !out_tokens) return fail(NSD_ERR_NULL, "sample: NULL pointer argument");
   if ((uintptr_t)probs & 15) return fail(NSD_ERR_SHAPE, "sample: probs must be 16-byte aligned");
-  Args A{probs, nullptr, nullptr, uniforms, nullptr, vocab, 0, 0, row_stride, out_stride,
-         nullptr, nullptr, nullptr, out_tokens};
+  Args A{probs, nullptr, nullptr, uniforms, nullptr, n_rows, vocab, 0, 0, row_stride,
+         out_stride, nullptr, nullptr, nullptr, out_tokens};
   return launch(true, A, n_rows, workspace, workspace_bytes, stream, "sample");
 }

@@ -61,9 +61,10 @@
 #include "nsd_internal.h"
 
 #include <math.h>
-#include <stdlib.h>
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 
 namespace {
 
@@ -218,6 +219,17 @@ __device__ inline int request_at(const uint16_t* order, int i) {
   return FUSE ? (int)order[i] : i;
 }
 
+// Query rows of request r: [qo, qo + nq) from q_indptr, clamped into the
+// rows [0, total_q) that total_q = q_indptr[bs] gives q and out, and nq to at
+// most max_q.  A well-formed q_indptr (non-decreasing, q_indptr[0] = 0) is
+// unchanged by the clamps; any other contents still address rows of q and
+// out only.
+__device__ inline void q_rows(const int32_t* __restrict__ q_indptr, int r, int total_q,
+                              int max_q, int& qo, int& nq) {
+  qo = min(max(q_indptr[r], 0), total_q);
+  nq = max(0, min(min(q_indptr[r + 1] - qo, max_q), total_q - qo));
+}
+
 // One (request r, KV head g) item restricted to the spans [j0, j1) whose
 // start lies in a range.
 struct Item {
@@ -231,7 +243,7 @@ template <int NB, bool FUSE>
 __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
                                  const int32_t* __restrict__ stage_table, int pos, int r,
-                                 int g, int64_t pr, int64_t s, int64_t s1) {
+                                 int g, int64_t pr, int64_t s, int64_t s1, int total_q) {
   Item it;
   it.pos = pos;
   it.r = r;
@@ -242,8 +254,7 @@ __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ se
   it.arriving = FUSE && is_arriving(p, stage_table, r);
   it.base = (int64_t)p.num_kv_heads * pr + (int64_t)g * it.n;
   spans_in(it.base, it.n, s, s1, it.j0, it.j1);
-  it.qo = q_indptr[r];
-  it.nq = max(0, min(q_indptr[r + 1] - it.qo, p.max_q));
+  q_rows(q_indptr, r, total_q, p.max_q, it.qo, it.nq);
   it.rows = p.group * it.nq;
   it.win = it.L - it.nq;
   return it;
@@ -255,12 +266,12 @@ template <int NB, bool FUSE>
 __device__ inline Item next_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
                                  const int32_t* __restrict__ stage_table, const uint16_t* order,
-                                 const Item& it, int64_t s, int64_t s1) {
+                                 const Item& it, int64_t s, int64_t s1, int total_q) {
   const bool nr = it.g == p.num_kv_heads - 1;
   const int pos = nr ? it.pos + 1 : it.pos;
   return make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos,
                              nr ? uniform(request_at<FUSE>(order, pos)) : it.r, nr ? 0 : it.g + 1,
-                             nr ? it.pr + it.n : it.pr, s, s1);
+                             nr ? it.pr + it.n : it.pr, s, s1, total_q);
 }
 
 // Raw block-table entries of one span (scalar loads, checked later).
@@ -829,17 +840,18 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
   // the item holding span position s
   const int n0 = spans_of<NB>(clamp_len(p, seq_lens, r0));
   const int g0 = (int)min((int64_t)hkv - 1, (s - (int64_t)hkv * pr0) / n0);
-  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos0, r0, g0, pr0, s, s1);
+  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos0, r0, g0, pr0, s, s1,
+                                total_q);
   if (it.j0 >= it.j1) {
     if (it.pos == p.bs - 1 && it.g == hkv - 1) return;
-    it = next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, it, s, s1);
+    it = next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, it, s, s1, total_q);
     if (it.j0 >= it.j1) return;   // no span lies in this range
   }
   // next item with a span in the range (or `it` itself when none)
   auto following = [&](const Item& cur) {
     const bool last = cur.pos == p.bs - 1 && cur.g == hkv - 1;
     if (last || cur.base + (int64_t)cur.n >= s1) return cur;
-    return next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, cur, s, s1);
+    return next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, cur, s, s1, total_q);
   };
   Item next = following(it);
   bool more = next.base != it.base;
@@ -1030,12 +1042,20 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
     }
   }
   __syncthreads();
-  if (total_q <= 0) return;   // no query rows: nothing to attend
 
   const int64_t hkv = p.num_kv_heads;
   const int64_t ta = hkv * s_pre[n_res], tb = hkv * s_pre[p.bs] - ta;
-  const int64_t W = waves_for<NB, FUSE>(ta + tb, p.num_waves);
   const int64_t rid = (int64_t)blockIdx.x * 4 + wave;
+  if (total_q <= 0) {
+    // no query rows: nothing to attend, but the arriving requests' blocks
+    // still move to the worker pool (the preparation does not depend on the
+    // queries), copied by every wave
+    if (FUSE && tb > 0)
+      copy_staged<D, NB>(p, block_table, stage_table, seq_lens, s_pre, s_order, (int)n_res, rid,
+                         p.num_waves, lane);
+    return;
+  }
+  const int64_t W = waves_for<NB, FUSE>(ta + tb, p.num_waves);
   // a batch too small for every resident wave: the surplus waves write the
   // staged blocks to the worker pool, so the attention waves stream without
   // stores, when there are enough of them and the batch is small enough for
@@ -1097,8 +1117,8 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
                  seg_b ? p.w_odd_b : p.w_odd);
   const int L = clamp_len(p, p.seq_lens, r);
   const int n = spans_of<NB>(L);
-  const int qo = p.q_indptr[r];
-  const int nq = max(0, min(p.q_indptr[r + 1] - qo, p.max_q));
+  int qo, nq;
+  q_rows(p.q_indptr, r, max(0, p.q_indptr[p.bs]), p.max_q, qo, nq);
   const int64_t base = (int64_t)p.prefix[pos] * hkv + (int64_t)g * n;
   const int64_t ra = uniform64(R.of(base - off));           // first span's range
   const int64_t rb = uniform64(R.of(base - off + n - 1));   // last span's range
@@ -1214,25 +1234,62 @@ struct Plan {
   size_t prefix_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
 };
 
-// Waves the device keeps resident for this kernel (CUs x waves per CU), or
-// NSD_ATTN_WAVES when set (a multiple of 4, for tests and tuning).
-int resident_waves(int d, int mt, bool fuse) {
-  const char* env = getenv("NSD_ATTN_WAVES");
-  if (env) {
-    const int v = atoi(env);
-    if (v >= 4 && v % 4 == 0) return v;
-  }
-  int dev = 0, cus = 0, blocks = 0;
-  const void* k = fuse ? kernel_for<true>(d, mt) : kernel_for<false>(d, mt);
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, 256, 0) != hipSuccess ||
-      cus <= 0 || blocks <= 0) {
+// Launch facts of one kernel instantiation on one device, queried once per
+// (device, instantiation) and kept for the process: the waves the device
+// keeps resident (CUs x workgroups per CU x 4), the LDS a workgroup may use
+// and the kernel's static LDS.
+struct KernelInfo {
+  int waves;
+  int lds_max;
+  size_t static_lds;
+  bool ok;
+};
+
+constexpr int kMaxDevices = 64;
+std::mutex g_info_mu;
+KernelInfo g_info[kMaxDevices][2][2][4];   // [device][fuse][head_dim 128][mt - 1]
+bool g_info_set[kMaxDevices][2][2][4];
+// Test and tuning hook (nsd_set_attention_waves): a wave count replacing
+// the device's, 0 for the device's own.
+std::atomic<int> g_waves_override{0};
+
+KernelInfo kernel_info(int d, int mt, bool fuse) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
     (void)hipGetLastError();
-    cus = 256;
-    blocks = 2;
+    return KernelInfo{0, 0, 0, false};
   }
-  return cus * blocks * 4;
+  const int f = fuse ? 1 : 0, h = d == 128 ? 1 : 0, m = std::min(std::max(mt, 1), 4) - 1;
+  std::lock_guard<std::mutex> lock(g_info_mu);
+  if (g_info_set[dev][f][h][m]) return g_info[dev][f][h][m];
+  KernelInfo ki{0, 0, 0, false};
+  int cus = 0, blocks = 0;
+  hipFuncAttributes fa;
+  const void* k = fuse ? kernel_for<true>(d, mt) : kernel_for<false>(d, mt);
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, 256, 0) == hipSuccess &&
+      hipDeviceGetAttribute(&ki.lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
+          hipSuccess &&
+      hipFuncGetAttributes(&fa, k) == hipSuccess && cus > 0 && blocks > 0) {
+    ki.waves = cus * blocks * 4;
+    ki.static_lds = fa.sharedSizeBytes;
+    ki.ok = true;
+    g_info[dev][f][h][m] = ki;
+    g_info_set[dev][f][h][m] = true;
+  } else {
+    (void)hipGetLastError();
+  }
+  return ki;
+}
+
+// Waves a launch uses: the override when set, else the device's resident
+// waves (256 CUs x 2 workgroups when the device cannot be queried, which
+// only sizes a workspace query; a launch then fails on the LDS query).
+int resident_waves(int d, int mt, bool fuse) {
+  const int w = g_waves_override.load(std::memory_order_relaxed);
+  if (w > 0) return w;
+  const KernelInfo ki = kernel_info(d, mt, fuse);
+  return ki.ok ? ki.waves : 256 * 2 * 4;
 }
 
 bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool fuse,
@@ -1315,18 +1372,11 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
                 pl.ws_bytes, workspace ? workspace_bytes : (size_t)0);
   // dynamic LDS: the span prefix and work order, then one output buffer per
   // wave taking the rest of what a workgroup may have (at least one record)
-  int dev = 0, lds_max = 0;
-  hipFuncAttributes fa;
-  const void* kfn = fuse ? kernel_for<true>(head_dim, pl.mt) : kernel_for<false>(head_dim, pl.mt);
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
-          hipSuccess ||
-      hipFuncGetAttributes(&fa, kfn) != hipSuccess) {
-    (void)hipGetLastError();
-    return fail(NSD_ERR_HIP, "%s: the device's LDS size could not be queried", fn);
-  }
+  const KernelInfo ki = kernel_info(head_dim, pl.mt, fuse);
+  if (!ki.ok) return fail(NSD_ERR_HIP, "%s: the device's LDS size could not be queried", fn);
+  const int lds_max = ki.lds_max;
   const size_t pre_bytes = (pl.lds_bytes + 15) / 16 * 16;
-  const size_t fixed = fa.sharedSizeBytes + pre_bytes;
+  const size_t fixed = ki.static_lds + pre_bytes;
   const size_t per_wave = (size_t)lds_max > fixed ? ((size_t)lds_max - fixed) / 4 / 16 * 16 : 0;
   const size_t min_cap = head_dim == 64 ? out_record_bytes<64>(kOutP, 16)
                                         : out_record_bytes<128>(kOutP, 16);
@@ -1385,6 +1435,18 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
 }
 
 }  // namespace
+
+extern "C" nsd_status nsd_set_attention_waves(int32_t waves) {
+  if (waves < 0 || waves % 4 || waves > (1 << 20))
+    return nsd::fail(NSD_ERR_SHAPE, "set_attention_waves: waves must be 0 or a positive "
+                     "multiple of 4 up to 2^20 (got %d)", waves);
+  g_waves_override.store(waves, std::memory_order_relaxed);
+  return NSD_OK;
+}
+
+extern "C" int32_t nsd_attention_waves(void) {
+  return g_waves_override.load(std::memory_order_relaxed);
+}
 
 extern "C" size_t nsd_verify_attention_workspace_size(int32_t bs, int32_t num_q_heads,
                                                       int32_t num_kv_heads, int32_t head_dim,

@@ -12,11 +12,18 @@ append, single-query attention and sampling."""
 from . import (kv_gather, verify_attention, gather_verify_attention, spec_accept, kv_append,
                commit_lengths, sample, accept_workspace_size)
 
+# Batches below this many requests prepare with the separate gather even when a
+# stage table is given: there the fused pass is bound by each wave's chain of
+# span steps and measured slower than gather + attention (verify_8b-shaped
+# requests: 4 requests 68 against 50 us, 8 requests 78 against 54 us; from
+# about 16 requests on the fused pass is as fast or faster).
+FUSED_MIN_BATCH = 16
+
 
 def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_table, seq_lens,
                  q_indptr, max_q_per_seq, max_seq_len, accept=None, out=None, workspace=None,
                  scale=None, stage_table=None, window_kv=None, committed=None,
-                 append_tables=None, accept_workspace=None):
+                 append_tables=None, accept_workspace=None, prepare="auto"):
     """Run the round; returns (out, accepted_len, out_tokens).
 
     Pools and staging planes are stacked over layers ([layers][blocks][...]);
@@ -32,8 +39,18 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
     ``append_tables`` = fused_tables(block_table, stage_table), if given).  With
     acceptance and a ``committed`` int32 [bs] tensor, the committed lengths are
     written there; ``accept_workspace`` is spec_accept's workspace.
+
+    ``prepare``: "auto" lets a batch of fewer than FUSED_MIN_BATCH requests
+    given both a stage table and the (src_ids, dst_ids) pairs take the
+    separate gather (the caller states the two describe the same preparation,
+    with ids in range), the faster path for such batches; "fused" keeps the
+    fused pass whenever a stage table is given; "gather" always gathers first.
     """
-    if stage_table is None:
+    if prepare not in ("auto", "fused", "gather"):
+        raise ValueError(f"prepare must be 'auto', 'fused' or 'gather', not {prepare!r}")
+    if stage_table is not None and src_ids is not None and (
+            prepare == "gather" or (prepare == "auto" and seq_lens.numel() < FUSED_MIN_BATCH)):
+        stage_table = None
         kv_gather(k_stage, v_stage, k_pool, v_pool, src_ids, dst_ids)
     elif window_kv is not None:
         # fused preparation: an arriving request's blocks are still in the staging

@@ -23,9 +23,10 @@ def attention_ref(meta, layer, r, scale=None):
     k, v = logical_kv(meta, layer, r)
     a, b = int(meta.q_indptr[r]), int(meta.q_indptr[r + 1])
     scale = 1.0 / np.sqrt(cfg.head_dim) if scale is None else scale
+    # bf16 bytes to the host first, widened there (a quarter of the transfer)
     return oracle.attention.verify_attention_request(
-        layer.q[a:b].double().cpu().numpy(), k.double().cpu().numpy(),
-        v.double().cpu().numpy(), scale)
+        layer.q[a:b].cpu().double().numpy(), k.cpu().double().numpy(),
+        v.cpu().double().numpy(), scale)
 
 
 def check_attention(meta, layer, out, requests, scale=None):

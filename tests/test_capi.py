@@ -180,3 +180,93 @@ def test_probe_library_exports_and_validates():
     assert w(fake, 8, fake, 0, fake, fake, 1, 4, 1, fake, None) == 2     # empty destination
     assert w(fake, 8, fake, 8, fake, fake, -1, 4, 1, fake, None) == 2    # write_per < 0
     assert w(fake, 8, fake, 8, fake, fake, 1, 4, -1, fake, None) == 2    # steps < 0
+
+
+def test_attention_wave_hook(lib):
+    # the explicit wave-count hook replaces the device's count for the workspace query
+    import paper_2609_29364_amd as nsd
+    assert lib.nsd_attention_waves() == 0
+    assert lib.nsd_set_attention_waves(6) == 2 and lib.nsd_set_attention_waves(-4) == 2
+    assert lib.nsd_attention_waves() == 0
+    small = big = None
+    with nsd.attention_waves(8):
+        assert lib.nsd_attention_waves() == 8
+        small = lib.nsd_verify_attention_workspace_size(4, 4, 2, 64, 5, 256)
+        with nsd.attention_waves(64):
+            big = lib.nsd_verify_attention_workspace_size(4, 4, 2, 64, 5, 256)
+        assert lib.nsd_attention_waves() == 8
+    assert lib.nsd_attention_waves() == 0
+    assert 0 < small < big
+
+
+def _plan(cfg_name="tiny", **kw):
+    from workload import CONFIGS, custom_config, make_meta
+    cfg = custom_config(**kw) if kw else CONFIGS[cfg_name]
+    return make_meta(cfg)
+
+
+def _check(meta, **over):
+    import paper_2609_29364_amd as nsd
+    args = dict(block_table=meta.block_table, seq_lens=meta.seq_lens, q_indptr=meta.q_indptr,
+                num_blocks=meta.num_blocks, max_q_per_seq=meta.max_q,
+                max_seq_len=meta.max_seq_len, stage_table=meta.stage_table,
+                stage_num_blocks=meta.stage_num_blocks, total_q=meta.total_q)
+    args.update(over)
+    nsd.check_plan(**args)
+
+
+def test_check_plan_accepts_the_workloads(lib):
+    from workload import CONFIGS, make_meta
+    for name in CONFIGS:
+        meta = make_meta(CONFIGS[name])
+        _check(meta)                     # fused plan (stage table)
+        _check(meta, stage_table=None)   # plain attention plan
+
+
+def test_check_plan_rejects_each_violation(lib):
+    import numpy as np
+    import paper_2609_29364_amd as nsd
+    meta = _plan(seed=61, bs=6, k_lo=1, k_hi=5, n_arriving=3, pool_blocks=None)
+    cases = []
+    qi = meta.q_indptr.copy(); qi[0] = 1; cases.append(("q_indptr[0]", dict(q_indptr=qi)))
+    cases.append(("q has", dict(total_q=meta.total_q + 1)))
+    qi = meta.q_indptr.copy(); qi[2] = qi[1]; cases.append(("query rows", dict(q_indptr=qi)))
+    qi = meta.q_indptr.copy(); qi[3] = qi[2] - 1; cases.append(("query rows", dict(q_indptr=qi)))
+    cases.append(("query rows", dict(max_q_per_seq=int(np.diff(meta.q_indptr).max()) - 1)))
+    sl = meta.seq_lens.copy(); sl[1] = 0; cases.append(("seq_len", dict(seq_lens=sl)))
+    cases.append(("seq_len", dict(max_seq_len=int(meta.seq_lens.max()) - 1)))
+    bt = meta.block_table.copy(); bt[2, 0] = meta.num_blocks; cases.append(("pool id", dict(block_table=bt)))
+    bt = meta.block_table.copy(); bt[2, 0] = -1; cases.append(("pool id", dict(block_table=bt)))
+    bt = meta.block_table.copy(); bt[3, 0] = bt[4, 0]; cases.append(("used twice", dict(block_table=bt)))
+    arr = int(np.nonzero(meta.arriving)[0][0])
+    st = meta.stage_table.copy(); st[arr, 1] = meta.stage_num_blocks
+    cases.append(("staging id", dict(stage_table=st)))
+    others = np.nonzero(meta.arriving)[0]
+    st = meta.stage_table.copy(); st[others[1], 0] = st[others[0], 0]
+    cases.append(("staging block", dict(stage_table=st)))
+    for needle, over in cases:
+        with pytest.raises(nsd.NsdError) as e:
+            _check(meta, **over)
+        assert needle in str(e.value), (needle, str(e.value))
+    # a plain attention plan may share a pool block between requests (read only)
+    bt = meta.block_table.copy(); bt[3, 0] = bt[4, 0]
+    _check(meta, block_table=bt, stage_table=None)
+    # entries past a request's blocks are not checked
+    bt = meta.block_table.copy()
+    n0 = -(-int(meta.seq_lens[0]) // 16)
+    if n0 < bt.shape[1]:
+        bt[0, n0:] = -7
+        _check(meta, block_table=bt)
+
+
+def test_check_pairs(lib):
+    import numpy as np
+    import paper_2609_29364_amd as nsd
+    meta = _plan()
+    nsd.check_pairs(meta.src_ids, meta.dst_ids, meta.stage_num_blocks, meta.num_blocks)
+    nsd.check_pairs(np.zeros(0, np.int32), np.zeros(0, np.int32), 0, 0)
+    for needle, s, d in [("source id", [0, 9], [1, 2]), ("destination id", [0, 1], [1, 64]),
+                         ("named twice", [0, 1], [3, 3]), ("source id", [-1], [0])]:
+        with pytest.raises(nsd.NsdError) as e:
+            nsd.check_pairs(np.array(s), np.array(d), 9, 64)
+        assert needle in str(e.value)

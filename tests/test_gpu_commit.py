@@ -50,38 +50,57 @@ def test_commit_lengths_matches_oracle(device):
 
 
 def test_round_close_writes_back_the_suffix(device):
-    # round -> acceptance -> commit -> suffix writeback into the host arena
+    # round -> acceptance -> commit -> suffix writeback into the host arena, on the
+    # GPU; every expected value comes from the oracle on the generator's inputs:
+    # accepted lengths (oracle.accept), committed lengths (oracle.commit), the
+    # pool after the preparation (oracle.gather) and the suffix blocks
+    # (oracle.commit.writeback_pairs) copied into the arena as it was before
+    from paper_2609_29364_amd.hostkv import writeback_pairs
     cfg = custom_config(seed=43, bs=6, k_lo=2, k_hi=5, n_arriving=2, pool_blocks=None)
     meta = make_meta(cfg)
     lay = make_layer(cfg, meta, 0, "cpu")
     host = make_hostkv(cfg, meta, lay)
     arena0 = (u16(host.k).copy(), u16(host.v).copy())
+    host_len = meta.seq_lens - np.diff(meta.q_indptr)      # the window is new this round
+    acc_cpu = make_accept(cfg, meta, "cpu")
+    # GPU: the worker's order of calls; the writeback plan follows the GPU's own lengths
     kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
     nsd.kv_gather(lay.k_stage.to(device), lay.v_stage.to(device), kp, vp,
                   i32(meta.src_ids, device), i32(meta.dst_ids, device))
-    acc_in = make_accept(cfg, meta, device)
-    acc, _ = nsd.spec_accept(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens,
-                             acc_in.uniforms, i32(meta.q_indptr, device), int(meta.depth.max()))
+    acc, _ = nsd.spec_accept(acc_cpu.p_target.to(device), acc_cpu.q_draft.to(device),
+                             acc_cpu.draft_tokens.to(device), acc_cpu.uniforms.to(device),
+                             i32(meta.q_indptr, device), int(meta.depth.max()))
     new_len = nsd.commit_lengths(i32(meta.seq_lens, device), i32(meta.q_indptr, device), acc)
     torch.cuda.synchronize()
-    new_len = new_len.cpu().numpy()
-    host_len = meta.seq_lens - (np.diff(meta.q_indptr))      # the window is new this round
-    src, dst = oracle.commit.writeback_pairs(meta.block_table, host.extent, host_len, new_len)
+    src, dst = writeback_pairs(meta.block_table, host.extent, host_len, new_len.cpu().numpy())
     nsd.kv_writeback(kp, vp, host.k, host.v, i32(src, device), i32(dst, device))
     torch.cuda.synchronize()
-    pool_k, pool_v = u16(kp.cpu()), u16(vp.cpu())
+    # oracle, from the generator's inputs only
+    n_ref, _ = oracle.accept.spec_accept(acc_cpu.p_target.numpy(), acc_cpu.q_draft.numpy(),
+                                         acc_cpu.draft_tokens.numpy(), acc_cpu.uniforms.numpy(),
+                                         meta.q_indptr)
+    len_ref = oracle.commit.commit_lengths(meta.seq_lens, meta.q_indptr, n_ref)
+    pool_k, pool_v = oracle.gather.kv_gather(u16(lay.k_stage)[None], u16(lay.v_stage)[None],
+                                             u16(lay.k_pool)[None], u16(lay.v_pool)[None],
+                                             meta.src_ids, meta.dst_ids)
+    s_ref, d_ref = oracle.commit.writeback_pairs(meta.block_table, host.extent, host_len,
+                                                 len_ref)
     ref_k, ref_v = arena0[0].copy(), arena0[1].copy()
-    ref_k[dst], ref_v[dst] = pool_k[src], pool_v[src]
+    ref_k[d_ref], ref_v[d_ref] = pool_k[0][s_ref], pool_v[0][s_ref]
+    assert np.array_equal(acc.cpu().numpy(), n_ref)
+    assert np.array_equal(new_len.cpu().numpy(), len_ref)
     assert np.array_equal(u16(host.k), ref_k) and np.array_equal(u16(host.v), ref_v)
-    # the arena now holds every request's committed tokens
+    assert len(s_ref) > 0
+    # the arena now holds every request's committed tokens (the generator's logical cache)
     from workload.layout import logical_kv_from_blocks
     from workload.synth import logical_kv
     for r in range(meta.bs):
-        n = -(-int(new_len[r]) // 16)
+        n = -(-int(len_ref[r]) // 16)
         e = int(host.extent[r])
-        k, v = logical_kv_from_blocks(host.k[e:e + n], host.v[e:e + n], int(new_len[r]))
+        k, v = logical_kv_from_blocks(host.k[e:e + n], host.v[e:e + n], int(len_ref[r]))
         k0, v0 = logical_kv(meta, lay, r)
-        assert torch.equal(k.view(torch.int16), k0[:int(new_len[r])].view(torch.int16))
+        assert torch.equal(k.view(torch.int16), k0[:int(len_ref[r])].view(torch.int16))
+        assert torch.equal(v.view(torch.int16), v0[:int(len_ref[r])].view(torch.int16))
 
 
 def test_host_alias_refuses_pageable(device):
@@ -128,9 +147,15 @@ def test_round_with_window_append(device, fused):
         meta.max_q, meta.max_seq_len,
         accept=(acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens, acc_in.uniforms,
                 int(meta.depth.max())),
-        stage_table=st, window_kv=[(kn.to(device), vn.to(device))], committed=committed)
+        stage_table=st, window_kv=[(kn.to(device), vn.to(device))], committed=committed,
+        prepare="fused" if fused else "gather")
     torch.cuda.synchronize()
     from parity import check_attention
     check_attention(meta, lay, outs[0], range(meta.bs))
-    ref = oracle.commit.commit_lengths(meta.seq_lens, meta.q_indptr, acc.cpu().numpy())
+    a = make_accept(cfg, meta, "cpu")
+    n_ref, _ = oracle.accept.spec_accept(a.p_target.numpy(), a.q_draft.numpy(),
+                                         a.draft_tokens.numpy(), a.uniforms.numpy(),
+                                         meta.q_indptr)
+    ref = oracle.commit.commit_lengths(meta.seq_lens, meta.q_indptr, n_ref)
+    assert np.array_equal(acc.cpu().numpy(), n_ref)
     assert np.array_equal(committed.cpu().numpy(), ref)

@@ -13,7 +13,7 @@ import paper_2609_29364_amd as nsd
 from paper_2609_29364_amd.round import draft_stage
 from workload import CONFIGS, custom_config, make_draft
 from workload.synth import logical_kv
-from parity import ATTN_ATOL, check_samples, i32
+from parity import ATTN_ATOL, check_accept, check_samples, i32
 
 pytestmark = pytest.mark.gpu
 
@@ -161,6 +161,19 @@ def test_draft_tokens_feed_acceptance(device):
     acc, out = nsd.spec_accept(p.to(device), dd.probs.view(-1, vocab), tok.view(-1),
                                u.to(device), i32(qi, device), k)
     torch.cuda.synchronize()
-    ref_acc, _ = oracle.accept.spec_accept(p.numpy(), dd.probs.view(-1, vocab).cpu().numpy(),
-                                           tok.view(-1).cpu().numpy(), u.numpy(), qi)
+    # the oracle draws the proposals itself from the generator's draft rows and
+    # uniforms, then accepts them: nothing it receives came from the library
+    rows = dd.probs.cpu().numpy()                                   # [bs][K][V]
+    x_ref = oracle.draft.sample(rows.reshape(-1, vocab),
+                                dd.uniforms.cpu().numpy().T.reshape(-1)).reshape(cfg.bs, k)
+    tok_gpu = tok.cpu().numpy()
+    # proposals equal except within the CDF-boundary tolerance (checked by check_samples)
+    check_samples(rows.reshape(-1, vocab), dd.uniforms.cpu().numpy().T.reshape(-1),
+                  tok_gpu.reshape(-1))
+    same = [r for r in range(cfg.bs) if np.array_equal(tok_gpu[r], x_ref[r])]
+    assert len(same) == cfg.bs
+    ref_acc, ref_tok = oracle.accept.spec_accept(p.numpy(), rows.reshape(-1, vocab),
+                                                 x_ref.reshape(-1).astype(np.int32), u.numpy(), qi)
+    check_accept(p.numpy(), rows.reshape(-1, vocab), x_ref.reshape(-1).astype(np.int32),
+                 u.numpy(), qi, acc.cpu().numpy(), out.cpu().numpy())
     assert np.array_equal(acc.cpu().numpy(), ref_acc)

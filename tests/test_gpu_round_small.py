@@ -2,8 +2,7 @@
 plus edge cases (ragged depths, L mod 16 in {0, 1, 15}, L = n_q, every GQA
 group size, both head dims).  The attention's work decomposition is forced
 through few waves (most items whole) and the device's full wave count (most
-items cut into partials) via NSD_ATTN_WAVES."""
-import os
+items cut into partials) through the library's wave-count hook."""
 
 import numpy as np
 import pytest
@@ -11,14 +10,14 @@ import torch
 
 import oracle
 import paper_2609_29364_amd as nsd
-from paper_2609_29364_amd.round import verify_round
+from paper_2609_29364_amd.round import verify_round, FUSED_MIN_BATCH
 from workload import CONFIGS, custom_config, make_meta, make_layer, make_accept
 from parity import i32, u16, check_attention, check_accept
 
 pytestmark = pytest.mark.gpu
 
 
-def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None, fused=False):
+def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None, fused=False, prepare=None):
     layers = layers or [make_layer(cfg, meta, l, "cpu") for l in range(cfg.num_layers)]
     stack = lambda name: torch.stack([getattr(l, name) for l in layers]).to(dev).contiguous()
     kp, vp, ks, vs, q = (stack(n) for n in ("k_pool", "v_pool", "k_stage", "v_stage", "q"))
@@ -27,23 +26,15 @@ def _run_round(cfg, meta, dev, layers=None, accept=True, waves=None, fused=False
     if acc_in is not None:
         acc_dev = (acc_in.p_target.to(dev), acc_in.q_draft.to(dev), acc_in.draft_tokens.to(dev),
                    acc_in.uniforms.to(dev), int(meta.depth.max()))
-    old = os.environ.get("NSD_ATTN_WAVES")
-    if waves:
-        os.environ["NSD_ATTN_WAVES"] = str(waves)
-    try:
-        st = i32(meta.stage_table, dev) if fused else None
+    with nsd.attention_waves(waves):
+        prepare = prepare or ("fused" if fused else "gather")
+        st = i32(meta.stage_table, dev) if prepare != "gather" else None
         outs, acc, tok = verify_round(kp, vp, ks, vs, i32(meta.src_ids, dev),
                                       i32(meta.dst_ids, dev), q, i32(meta.block_table, dev),
                                       i32(meta.seq_lens, dev), i32(meta.q_indptr, dev),
                                       meta.max_q, meta.max_seq_len, accept=acc_dev,
-                                      stage_table=st)
+                                      stage_table=st, prepare=prepare)
         torch.cuda.synchronize()
-    finally:
-        if waves:
-            if old is None:
-                del os.environ["NSD_ATTN_WAVES"]
-            else:
-                os.environ["NSD_ATTN_WAVES"] = old
     return layers, kp, vp, outs, acc_in, acc, tok
 
 
@@ -241,10 +232,7 @@ def test_workspace_reuse(device, waves):
                         ctx_lo=300, ctx_hi=1200, k_lo=2, k_hi=2, n_arriving=2, pool_blocks=None)
     meta = make_meta(cfg)
     lay = make_layer(cfg, meta, 0, "cpu")
-    old = os.environ.get("NSD_ATTN_WAVES")
-    if waves:
-        os.environ["NSD_ATTN_WAVES"] = str(waves)
-    try:
+    with nsd.attention_waves(waves):
         n = nsd.verify_attention_workspace_size(cfg.bs, cfg.num_q_heads, cfg.num_kv_heads,
                                                 cfg.head_dim, meta.max_q, meta.max_seq_len)
         ws = nsd.new_workspace(n, device)
@@ -267,12 +255,6 @@ def test_workspace_reuse(device, waves):
                                          workspace=ws)
             torch.cuda.synchronize()
             outs.append(o.clone())
-    finally:
-        if waves:
-            if old is None:
-                del os.environ["NSD_ATTN_WAVES"]
-            else:
-                os.environ["NSD_ATTN_WAVES"] = old
     assert torch.equal(outs[1].view(torch.int16), outs[2].view(torch.int16))
     assert torch.equal(outs[0].view(torch.int16), outs[3].view(torch.int16))
     for o in outs:
@@ -507,3 +489,36 @@ def test_first_token_follows_target_row(device):
     r64 = p0.astype(np.float64)
     assert stats.chisquare(counts, r64 / r64.sum() * bs).pvalue > 1e-4
     check_accept(p, q, x, u, q_indptr, acc, tok, requests=range(0, bs, 97))
+
+
+@pytest.mark.parametrize("bs", [FUSED_MIN_BATCH - 1, FUSED_MIN_BATCH])
+def test_auto_preparation_both_sides_of_the_threshold(device, bs):
+    # verify_round's default preparation: below FUSED_MIN_BATCH requests the
+    # separate gather, from it on the fused pass; both against the oracle
+    cfg = custom_config(seed=70 + bs, bs=bs, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                        ctx_lo=200, ctx_hi=1500, k_lo=4, k_hi=4, n_arriving=bs // 3,
+                        vocab=1000, pool_blocks=None)
+    meta = make_meta(cfg)
+    _check_all(cfg, meta, device, prepare="auto")
+
+
+def test_fused_without_query_rows_still_prepares(device):
+    # q_indptr all zero (no query rows): the fused call has nothing to attend,
+    # but it still moves the arriving requests' blocks into the pool, as the
+    # separate gather does
+    cfg = custom_config(seed=75, bs=7, n_arriving=3, pool_blocks=None, vocab=0)
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, 0, "cpu")
+    kp, vp = lay.k_pool.to(device), lay.v_pool.to(device)
+    # one row of q and out (an empty tensor has no address); none is read or written
+    q0 = torch.zeros((1, cfg.num_q_heads, cfg.head_dim), dtype=torch.bfloat16, device=device)
+    qi = torch.zeros(cfg.bs + 1, dtype=torch.int32, device=device)
+    out = nsd.gather_verify_attention(q0, kp, vp, lay.k_stage.to(device), lay.v_stage.to(device),
+                                      i32(meta.block_table, device),
+                                      i32(meta.stage_table, device), i32(meta.seq_lens, device),
+                                      qi, meta.max_q, meta.max_seq_len)
+    torch.cuda.synchronize()
+    ref_k, ref_v = oracle.gather.kv_gather(u16(lay.k_stage)[None], u16(lay.v_stage)[None],
+                                           u16(lay.k_pool)[None], u16(lay.v_pool)[None],
+                                           meta.src_ids, meta.dst_ids)
+    assert np.array_equal(u16(kp), ref_k[0]) and np.array_equal(u16(vp), ref_v[0])

@@ -1,12 +1,16 @@
 """GPU parity at the named workloads' full sizes, in the launch configuration the
 benchmark times (default decomposition, one stream, gather -> attention ->
-accept).  The oracle checks what it can compute at these sizes: the gather
-bytewise (whole pool, or every destination block plus sampled canary blocks),
-attention on sampled requests (shortest, longest, arriving and resident, plus
-random ones), and acceptance on every request.
+accept).  Against the oracle: the gather bytewise (whole pool, or every
+destination block plus sampled canary blocks), attention on every request
+(draft_decode, verify_8b, knee), and acceptance on every request.
 
 The 36-layer round does not fit in HBM at once (about 650 GB of KV); it is
-checked layer by layer on layers 0, 17 and 35."""
+checked layer by layer, on all 36 layers, in the fused pass the benchmark
+times: attention on four requests per layer (shortest, longest, an arriving
+and a resident one, rotated with the layer); the gather on every destination
+block of layers 0, 17 and 35 and, on the other layers, every destination
+block of four arriving requests, each with 2000 sampled canary blocks.
+Layers 0 and 35 also run the separate gather + attention."""
 import numpy as np
 import pytest
 import torch
@@ -34,8 +38,10 @@ def _sample_requests(meta, k=6, seed=0):
     return sorted(picks)
 
 
-def _gather_check(meta, lay, kp, vp, full, seed=0):
-    """Bytewise check of the worker pool after the gather against the oracle."""
+def _gather_check(meta, lay, kp, vp, full, seed=0, dst_subset=None, n_canary=4000):
+    """Bytewise check of the worker pool after the gather against the oracle.
+    full: the whole pool; else every destination block (or the pairs listed in
+    dst_subset) plus n_canary sampled blocks no pair names."""
     u16 = lambda t: t.view(torch.int16)
     if full:
         ref_k, ref_v = oracle.gather.kv_gather(
@@ -47,18 +53,24 @@ def _gather_check(meta, lay, kp, vp, full, seed=0):
         return
     # every destination block, plus sampled blocks no pair names (canaries)
     rng = np.random.default_rng(seed)
+    pairs = np.arange(len(meta.dst_ids)) if dst_subset is None else np.asarray(dst_subset)
+    src_ids, dst_ids = meta.src_ids[pairs], meta.dst_ids[pairs]
     dst = set(meta.dst_ids.tolist())
-    others = np.array([b for b in rng.choice(meta.num_blocks, 4000, replace=False) if b not in dst])
-    blocks = np.concatenate([meta.dst_ids, others]).astype(np.int64)
+    others = np.array([b for b in rng.choice(meta.num_blocks, n_canary, replace=False)
+                       if b not in dst], dtype=np.int64)
+    blocks = np.concatenate([dst_ids, others]).astype(np.int64)
     idx = torch.as_tensor(blocks, device=kp.device)
-    # the oracle sees only the listed blocks: its plan maps staging ids to positions
+    # the oracle sees only the listed blocks: its plan maps pool ids to positions,
+    # and the staging blocks the pairs name, in pair order
     pos = {int(b): i for i, b in enumerate(blocks)}
     sub_k0 = u16(lay.k_pool[idx]).cpu().numpy()[None]
     sub_v0 = u16(lay.v_pool[idx]).cpu().numpy()[None]
-    sub_dst = np.array([pos[int(d)] for d in meta.dst_ids])
-    ref_k, ref_v = oracle.gather.kv_gather(u16(lay.k_stage).cpu().numpy()[None],
-                                           u16(lay.v_stage).cpu().numpy()[None], sub_k0, sub_v0,
-                                           meta.src_ids, sub_dst)
+    sub_dst = np.array([pos[int(d)] for d in dst_ids], dtype=np.int64)
+    sidx = torch.as_tensor(src_ids.astype(np.int64), device=kp.device)
+    stg_k = u16(lay.k_stage[sidx]).cpu().numpy()[None]
+    stg_v = u16(lay.v_stage[sidx]).cpu().numpy()[None]
+    ref_k, ref_v = oracle.gather.kv_gather(stg_k, stg_v, sub_k0, sub_v0,
+                                           np.arange(len(src_ids)), sub_dst)
     assert np.array_equal(u16(kp[idx]).cpu().numpy(), ref_k[0])
     assert np.array_equal(u16(vp[idx]).cpu().numpy(), ref_v[0])
 
@@ -92,7 +104,7 @@ def _round(name, device, full_gather, fused):
     torch.cuda.synchronize()
     print(f"{name} (fused={fused}): round ran, checking", flush=True)
     _gather_check(meta, lay, kp, vp, full_gather)
-    worst = check_attention(meta, lay, out, _sample_requests(meta))
+    worst = check_attention(meta, lay, out, range(meta.bs))
     print(f"{name}: attention max abs error {worst:.3e}", flush=True)
     if acc_in is not None:
         near = check_accept(acc_in.p_target.cpu().numpy(), acc_in.q_draft.cpu().numpy(),
@@ -119,16 +131,56 @@ def test_knee_full(device, fused):
     _round("knee", device, full_gather=False, fused=fused)
 
 
-@pytest.mark.parametrize("layer,fused", [(0, False), (17, True), (35, False), (35, True)])
-def test_full_depth_layer(device, layer, fused):
+def _layer_requests(meta, layer):
+    """Four requests of a full-depth layer: the shortest and the longest, and an
+    arriving and a resident one chosen by the layer index."""
+    arr = np.nonzero(meta.arriving)[0]
+    res = np.nonzero(~meta.arriving)[0]
+    picks = {int(np.argmin(meta.seq_lens)), int(np.argmax(meta.seq_lens)),
+             int(arr[(7 * layer) % len(arr)]), int(res[(11 * layer) % len(res)])}
+    return sorted(picks)
+
+
+def _pairs_of(meta, requests):
+    """Indexes of the gather pairs that prepare the listed requests."""
+    starts = np.concatenate([[0], np.cumsum([meta.nblk(r) for r in np.nonzero(meta.arriving)[0]])])
+    order = {int(r): i for i, r in enumerate(np.nonzero(meta.arriving)[0])}
+    out = []
+    for r in requests:
+        i = order[int(r)]
+        out.extend(range(int(starts[i]), int(starts[i + 1])))
+    return np.array(out, dtype=np.int64)
+
+
+@pytest.mark.parametrize("layer", range(36))
+def test_full_depth_layer(device, layer):
     cfg = CONFIGS["full_depth"]
     meta = make_meta(cfg)
     lay = make_layer(cfg, meta, layer, device)
-    kp, vp, out = _attend(meta, lay, device, fused)
+    kp, vp, out = _attend(meta, lay, device, fused=True)
     torch.cuda.synchronize()
-    _gather_check(meta, lay, kp, vp, full=False, seed=layer)
-    worst = check_attention(meta, lay, out, _sample_requests(meta, k=2, seed=layer))
+    print(f"full_depth layer {layer}: fused pass ran, checking", flush=True)
+    if layer in (0, 17, 35):
+        _gather_check(meta, lay, kp, vp, full=False, seed=layer, n_canary=2000)
+    else:
+        arr = np.nonzero(meta.arriving)[0]
+        pick = [int(arr[(layer * 5 + i * 13) % len(arr)]) for i in range(4)]
+        _gather_check(meta, lay, kp, vp, full=False, seed=layer, n_canary=2000,
+                      dst_subset=_pairs_of(meta, sorted(set(pick))))
+    worst = check_attention(meta, lay, out, _layer_requests(meta, layer))
     print(f"full_depth layer {layer}: attention max abs error {worst:.3e}", flush=True)
+
+
+@pytest.mark.parametrize("layer", [0, 35])
+def test_full_depth_layer_unfused(device, layer):
+    cfg = CONFIGS["full_depth"]
+    meta = make_meta(cfg)
+    lay = make_layer(cfg, meta, layer, device)
+    kp, vp, out = _attend(meta, lay, device, fused=False)
+    torch.cuda.synchronize()
+    _gather_check(meta, lay, kp, vp, full=False, seed=100 + layer, n_canary=2000)
+    worst = check_attention(meta, lay, out, _layer_requests(meta, layer + 1))
+    print(f"full_depth layer {layer} (unfused): attention max abs error {worst:.3e}", flush=True)
 
 
 def test_full_depth_accept(device):
