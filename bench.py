@@ -244,15 +244,48 @@ def practical_ceiling(dev, read_bytes, write_bytes, reps=7, placement="end"):
     return out
 
 
-def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
-    """The CPU oracle, untuned, on a bounded sample of the same round."""
-    import oracle
-    from workload.synth import logical_kv
+def host_facts():
+    """The host the oracle runs on: usable cores, CPU model, BLAS pool size."""
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        cores = os.cpu_count() or 1
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = 1
+        blas = 1
+    return {"host_cores": cores, "cpu_model": model, "blas_threads": int(blas),
+            "nproc": os.cpu_count()}
+
+
+def cpu_baseline(cfg, meta, layer, acc_in, budget_s, threads=None):
+    """The CPU oracle, untuned, on a bounded sample of the same round.
+
+    threads: None runs with the BLAS pool the host provides; an integer limits
+    it (threadpoolctl) for the duration of the sample."""
+    import contextlib
+    import oracle
+    from workload.synth import logical_kv
+    facts = host_facts()
+    limit = contextlib.nullcontext()
+    if threads is not None:
+        from threadpoolctl import threadpool_limits
+        limit = threadpool_limits(limits=int(threads))
+    with limit:
+        return _cpu_baseline(cfg, meta, layer, acc_in, budget_s, facts,
+                             facts["blas_threads"] if threads is None else int(threads))
+
+
+def _cpu_baseline(cfg, meta, layer, acc_in, budget_s, facts, threads):
     rng = np.random.default_rng(0)
     order = rng.permutation(cfg.bs)
     p = acc_in.p_target if acc_in is not None else None
@@ -266,9 +299,9 @@ def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
         # host copies of this request's inputs (not timed)
         nb = meta.nblk(r)
         k, v = logical_kv(meta, layer, r)
-        k64, v64 = k.double().cpu().numpy(), v.double().cpu().numpy()
+        k64, v64 = k.cpu().double().numpy(), v.cpu().double().numpy()
         a, b = int(meta.q_indptr[r]), int(meta.q_indptr[r + 1])
-        q64 = layer.q[a:b].double().cpu().numpy()
+        q64 = layer.q[a:b].cpu().double().numpy()
         if meta.arriving[r]:
             ids = meta.stage_table[r, :nb]
             sk, sv = u16(layer.k_stage[ids])[None], u16(layer.v_stage[ids])[None]
@@ -296,7 +329,9 @@ def cpu_baseline(cfg, meta, layer, acc_in, budget_s):
     # stands for every layer) and accepts once
     per_req = (t_layer * cfg.num_layers + t_acc) / done
     return {"value": round(1.0 / per_req, 3), "unit": "requests/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "host_cores": facts["host_cores"], "cpu_model": facts["cpu_model"],
+            "threads_note": "cores = the BLAS threads the fp64 numpy oracle may use; the "
+                            "oracle's own loops run on one Python thread",
             "sample": (f"{done} of {cfg.bs} requests" if done <= cfg.bs else
                        f"{done} requests ({done / cfg.bs:.1f} passes over the {cfg.bs})")
                       + f" of the {cfg.name} round (gather of their "
@@ -891,7 +926,7 @@ def sweep_bench(args):
                "bytes": alg,
                "fused_tbs": round(alg["fused"] / (fused_ms * 1e-3) / 1e12, 3),
                "fused_frac": round(alg["fused"] / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-               "gather_attention_tbs": round((alg["gather"] + alg["attention"]) /
+               "gather_attention_equiv_tbs": round((alg["gather"] + alg["attention"]) /
                                              (fused_ms * 1e-3) / 1e12, 3),
                "accept_tbs": (round(alg["accept"] / (acc_ms * 1e-3) / 1e12, 3)
                               if acc_ms > 0 else None),
@@ -1003,6 +1038,32 @@ def main():
     parts = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
                       for e in evs])
     g_ms, a_ms, c_ms = parts.mean(0)
+    # per-step spread, and the same steps after an untimed 1 GiB write that
+    # evicts the 256 MB last-level cache (MALL) before each step: the A/B shows
+    # how much of the back-to-back figure any cache carry-over could explain
+    scrub = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+
+    def per_step(scrubbed):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        for i in range(args.steps):
+            if scrubbed:
+                scrub.fill_(i & 0xFF)
+            ev[i][0].record(stream)
+            step()
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in ev])
+
+    t_plain, t_scrub = per_step(False), per_step(True)
+    del scrub
+    spread = {"median": round(float(np.median(t_plain)), 5),
+              "min": round(float(t_plain.min()), 5), "max": round(float(t_plain.max()), 5),
+              "median_scrubbed": round(float(np.median(t_scrub)), 5),
+              "min_scrubbed": round(float(t_scrub.min()), 5),
+              "max_scrubbed": round(float(t_scrub.max()), 5),
+              "scrub_bytes": 1 << 30,
+              "scrub_effect": round(float(np.median(t_scrub) / np.median(t_plain) - 1.0), 4)}
     acc_host = acc_len.cpu().numpy() if acc_in is not None else None
     alg = algorithmic_bytes(cfg, meta, acc_host)
     # the dominant kernel: the fused pass, or attention when run unfused
@@ -1022,11 +1083,12 @@ def main():
         "path": "unfused" if args.unfused else "fused",
         "breakdown_ms": ({"kv_gather": round(g_ms, 5)} if args.unfused else {}) |
                         {kern: round(a_ms, 5), "spec_accept": round(c_ms, 5)},
+        "step_ms": spread,
         "round_hbm_tbs": round(step_bytes / (ms_step * 1e-3) / 1e12, 3),
-        # the KV-state preparation plus attention work, counted as the two
-        # separate kernels would move it, over the time the path took for it
-        "gather_attention_tbs": round((alg["gather"] + alg["attention"]) /
-                                      ((g_ms + a_ms) * 1e-3) / 1e12, 3),
+        # an equivalent rate, not an HBM rate: the bytes the separate gather and
+        # attention kernels would move, over the time this path took for that work
+        "gather_attention_equiv_tbs": round((alg["gather"] + alg["attention"]) /
+                                            ((g_ms + a_ms) * 1e-3) / 1e12, 3),
         "roofline": {"bound": "hbm", "kernel": kern, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -1044,7 +1106,19 @@ def main():
                                            "read_only_gbs": ceil["read_only_gbs"],
                                            "pattern": ceil["pattern"]}
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cfg, meta, layer, acc_in, args.cpu_seconds)
+        base = cpu_baseline(cfg, meta, layer, acc_in, args.cpu_seconds)
+        # one-thread figures on this workload and on the tiny round
+        one = {cfg.name: cpu_baseline(cfg, meta, layer, acc_in, args.cpu_seconds / 3,
+                                      threads=1)["value"]}
+        tcfg = CONFIGS["tiny"]
+        tmeta = make_meta(tcfg)
+        tlay = make_layer(tcfg, tmeta, 0, dev)
+        tacc = make_accept(tcfg, tmeta, dev)
+        tiny = cpu_baseline(tcfg, tmeta, tlay, tacc, 1.0)
+        one["tiny"] = cpu_baseline(tcfg, tmeta, tlay, tacc, 1.0, threads=1)["value"]
+        base["one_thread_requests_per_s"] = one
+        base["tiny_requests_per_s"] = tiny["value"]
+        result["cpu_baseline"] = base
     print(json.dumps(result), flush=True)
 
 

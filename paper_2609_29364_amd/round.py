@@ -51,6 +51,7 @@ def verify_round(k_pool, v_pool, k_stage, v_stage, src_ids, dst_ids, q, block_ta
     if stage_table is not None and src_ids is not None and (
             prepare == "gather" or (prepare == "auto" and seq_lens.numel() < FUSED_MIN_BATCH)):
         stage_table = None
+    if stage_table is None:
         kv_gather(k_stage, v_stage, k_pool, v_pool, src_ids, dst_ids)
     elif window_kv is not None:
         # fused preparation: an arriving request's blocks are still in the staging
