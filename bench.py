@@ -273,8 +273,6 @@ def cpu_baseline(cfg, meta, layer, acc_in, budget_s, threads=None):
     threads: None runs with the BLAS pool the host provides; an integer limits
     it (threadpoolctl) for the duration of the sample."""
     import contextlib
-    import oracle
-    from workload.synth import logical_kv
     facts = host_facts()
     limit = contextlib.nullcontext()
     if threads is not None:
@@ -286,6 +284,8 @@ def cpu_baseline(cfg, meta, layer, acc_in, budget_s, threads=None):
 
 
 def _cpu_baseline(cfg, meta, layer, acc_in, budget_s, facts, threads):
+    import oracle
+    from workload.synth import logical_kv
     rng = np.random.default_rng(0)
     order = rng.permutation(cfg.bs)
     p = acc_in.p_target if acc_in is not None else None

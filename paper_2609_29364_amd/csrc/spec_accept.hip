@@ -137,45 +137,107 @@ __device__ inline const float* row_p(const Args& A, int r, int a, int n) {
   return SAMPLE ? A.p + (int64_t)r * A.row_stride : A.p + (int64_t)(a + n) * A.vocab;
 }
 
-// Sums of chunks [c_beg, c_end) of the weight row into dst[c], by the NW
-// waves of a workgroup.
-template <int NW>
-__device__ inline void chunk_sums(const float* prow, const float* qrow, bool resid, int vocab,
-                                  int c_beg, int c_end, int lane, int wave, double* dst) {
-  for (int c0 = c_beg + wave; c0 < c_end; c0 += NW * kUnroll) {
-    f32x4 pv[kUnroll], qv[kUnroll];
+// One iteration's loads: chunks c0 + u * NW (u < kUnroll) of the weight row,
+// one 16-byte load per lane and chunk (and the draft row's with RESID).
+// Without CHECK every chunk must be whole and inside [., c_end); with it,
+// chunks past c_end and elements past the vocabulary read as zero.
+template <bool RESID, bool CHECK, int NW>
+__device__ __attribute__((always_inline)) inline void load_chunks(const float* prow, const float* qrow, int vocab, int c0,
+                                   int c_end, int lane, f32x4 (&pv)[kUnroll],
+                                   f32x4 (&qv)[kUnroll]) {
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int c = c0 + u * NW;
-      const int idx = c * kChunk + lane * 4;
-      pv[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
-      qv[u] = pv[u];
-      if (c < c_end && idx < vocab) {
-        pv[u] = __builtin_nontemporal_load((const f32x4*)(prow + idx));
-        if (resid) qv[u] = __builtin_nontemporal_load((const f32x4*)(qrow + idx));
-      }
-    }
-    // the four chunk sums in one butterfly: halves of the lanes swap two
-    // chunks' values (xor 32), then one (xor 16), then 16-lane sums; lanes 0,
-    // 16, 32, 48 end with chunks 0, 1, 2, 3
-    double v[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      double w[4];
-      weights4(pv[u], qv[u], resid, w);
-      v[u] = ((w[0] + w[1]) + w[2]) + w[3];
-    }
-    const bool h5 = lane & 32, h4 = lane & 16;
-    const double r0 = (h5 ? v[2] : v[0]) + __shfl_xor(h5 ? v[0] : v[2], 32);
-    const double r1 = (h5 ? v[3] : v[1]) + __shfl_xor(h5 ? v[1] : v[3], 32);
-    double s = (h4 ? r1 : r0) + __shfl_xor(h4 ? r0 : r1, 16);
-#pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o);
-    if ((lane & 15) == 0) {
-      const int c = c0 + ((h5 ? 2 : 0) + (h4 ? 1 : 0)) * NW;
-      if (c < c_end) dst[c] = s;
+  for (int u = 0; u < kUnroll; ++u) {
+    const int c = c0 + u * NW;
+    const int idx = c * kChunk + lane * 4;
+    pv[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    qv[u] = pv[u];
+    if (!CHECK || (c < c_end && idx < vocab)) {
+      pv[u] = __builtin_nontemporal_load((const f32x4*)(prow + idx));
+      if (RESID) qv[u] = __builtin_nontemporal_load((const f32x4*)(qrow + idx));
     }
   }
+  // keep the reduction of the previous iteration after these loads: they go
+  // out first, so the wave always has an iteration's loads in flight
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// The four chunk sums of one iteration in one butterfly, into dst: halves of
+// the lanes swap two chunks' values (xor 32), then one (xor 16), then 16-lane
+// sums; lanes 0, 16, 32, 48 end with chunks 0, 1, 2, 3.
+template <bool RESID, int NW>
+__device__ __attribute__((always_inline)) inline void reduce_chunks(const f32x4 (&pv)[kUnroll], const f32x4 (&qv)[kUnroll],
+                                     int c0, int c_end, int lane, double* dst) {
+  double v[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    double w[4];
+    weights4(pv[u], qv[u], RESID, w);
+    v[u] = ((w[0] + w[1]) + w[2]) + w[3];
+  }
+  const bool h5 = lane & 32, h4 = lane & 16;
+  const double r0 = (h5 ? v[2] : v[0]) + __shfl_xor(h5 ? v[0] : v[2], 32);
+  const double r1 = (h5 ? v[3] : v[1]) + __shfl_xor(h5 ? v[1] : v[3], 32);
+  double s = (h4 ? r1 : r0) + __shfl_xor(h4 ? r0 : r1, 16);
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+  if ((lane & 15) == 0) {
+    const int c = c0 + ((h5 ? 2 : 0) + (h4 ? 1 : 0)) * NW;
+    if (c < c_end) dst[c] = s;
+  }
+}
+
+// Sums of chunks [c_beg, c_end) of the weight row into dst[c], by the NW
+// waves of a workgroup: wave w takes iterations of kUnroll chunks w, w + NW,
+// ...  The loads are double-buffered, so a wave always has the next
+// iteration's loads in flight while it reduces the current one.  Every
+// iteration but a wave's last covers whole chunks inside the range (only the
+// range's last chunk can be partial, and it falls in the last iteration of
+// the wave holding it), so the loop's loads are unconditional; the last
+// iteration's are checked.
+template <int NW, bool RESID>
+__device__ __attribute__((always_inline)) inline void chunk_sums_t(const float* prow, const float* qrow, int vocab, int c_beg,
+                                    int c_end, int lane, int wave, double* dst) {
+  constexpr int kStep = NW * kUnroll;
+  const int first = c_beg + wave;
+  if (first >= c_end) return;
+  const int n_iter = (c_end - first + kStep - 1) / kStep;
+  f32x4 pa[kUnroll], qa[kUnroll], pb[kUnroll], qb[kUnroll];
+  if (n_iter == 1) {
+    load_chunks<RESID, true, NW>(prow, qrow, vocab, first, c_end, lane, pa, qa);
+    reduce_chunks<RESID, NW>(pa, qa, first, c_end, lane, dst);
+    return;
+  }
+  // two register sets used in turn (unrolled by two, so no set is copied: a
+  // copy would wait for the loads still landing in it)
+  load_chunks<RESID, false, NW>(prow, qrow, vocab, first, c_end, lane, pa, qa);
+  int c0 = first, it = 0;
+  for (; it + 3 < n_iter; it += 2, c0 += 2 * kStep) {
+    load_chunks<RESID, false, NW>(prow, qrow, vocab, c0 + kStep, c_end, lane, pb, qb);
+    reduce_chunks<RESID, NW>(pa, qa, c0, c_end, lane, dst);
+    load_chunks<RESID, false, NW>(prow, qrow, vocab, c0 + 2 * kStep, c_end, lane, pa, qa);
+    reduce_chunks<RESID, NW>(pb, qb, c0 + kStep, c_end, lane, dst);
+  }
+  // two or three iterations left, the first of them loaded
+  if (n_iter - it == 3) {
+    load_chunks<RESID, false, NW>(prow, qrow, vocab, c0 + kStep, c_end, lane, pb, qb);
+    reduce_chunks<RESID, NW>(pa, qa, c0, c_end, lane, dst);
+    load_chunks<RESID, true, NW>(prow, qrow, vocab, c0 + 2 * kStep, c_end, lane, pa, qa);
+    reduce_chunks<RESID, NW>(pb, qb, c0 + kStep, c_end, lane, dst);
+    reduce_chunks<RESID, NW>(pa, qa, c0 + 2 * kStep, c_end, lane, dst);
+  } else {
+    load_chunks<RESID, true, NW>(prow, qrow, vocab, c0 + kStep, c_end, lane, pb, qb);
+    reduce_chunks<RESID, NW>(pa, qa, c0, c_end, lane, dst);
+    reduce_chunks<RESID, NW>(pb, qb, c0 + kStep, c_end, lane, dst);
+  }
+}
+
+template <int NW>
+__device__ __attribute__((always_inline)) inline void chunk_sums(const float* prow, const float* qrow, bool resid, int vocab,
+                                  int c_beg, int c_end, int lane, int wave, double* dst) {
+  if (resid)
+    chunk_sums_t<NW, true>(prow, qrow, vocab, c_beg, c_end, lane, wave, dst);
+  else
+    chunk_sums_t<NW, false>(prow, qrow, vocab, c_beg, c_end, lane, wave, dst);
 }
 static_assert(kUnroll == 4, "the butterfly in chunk_sums reduces four chunks");
 
@@ -454,29 +516,40 @@ extern "C" size_t nsd_spec_accept_workspace_size(int32_t rows, int32_t vocab) {
   return (size_t)(sums_bytes(rows, vocab) + (int64_t)rows * 4);
 }
 
+// Validation and launch of nsd_spec_accept.
+static nsd_status spec_accept_impl(const char* fn, const float* p_target, const float* q_draft,
+                            const int32_t* draft_tokens, const float* uniforms,
+                            const int32_t* q_indptr, int32_t bs, int32_t vocab, int32_t max_k,
+                            int32_t* accepted_len, int32_t* out_tokens, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  using namespace nsd;
+  if (bs < 0 || bs > kMaxRows)
+    return fail(NSD_ERR_SHAPE, "%s: bs must be in [0, %d]", fn, kMaxRows);
+  if (vocab < 4 || vocab > kMaxVocab || vocab % 4)
+    return fail(NSD_ERR_UNSUPPORTED, "%s: vocab must be a multiple of 4 in [4, %d] "
+                "(got %d)", fn, kMaxVocab, vocab);
+  if (max_k < 0 || max_k > kMaxK)
+    return fail(NSD_ERR_UNSUPPORTED, "%s: max_k must be in [0, %d] (got %d)", fn, kMaxK, max_k);
+  if (bs == 0) return NSD_OK;
+  if (!p_target || !uniforms || !q_indptr || !accepted_len || !out_tokens ||
+      (max_k > 0 && (!q_draft || !draft_tokens)))
+    return fail(NSD_ERR_NULL, "%s: NULL pointer argument", fn);
+  if (((uintptr_t)p_target | (uintptr_t)(max_k > 0 ? q_draft : p_target)) & 15)
+    return fail(NSD_ERR_SHAPE, "%s: probability rows must be 16-byte aligned", fn);
+  Args A{p_target, q_draft, draft_tokens, uniforms, q_indptr, bs, vocab, max_k, 0,
+         (int64_t)vocab, 1, nullptr, nullptr, accepted_len, out_tokens};
+  return launch(false, A, bs, workspace, workspace_bytes, stream, fn);
+}
+
 extern "C" nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
                                       const int32_t* draft_tokens, const float* uniforms,
                                       const int32_t* q_indptr, int32_t bs, int32_t vocab,
                                       int32_t max_k, int32_t* accepted_len,
                                       int32_t* out_tokens, void* workspace,
                                       size_t workspace_bytes, void* stream) {
-  using namespace nsd;
-  if (bs < 0 || bs > kMaxRows)
-    return fail(NSD_ERR_SHAPE, "spec_accept: bs must be in [0, %d]", kMaxRows);
-  if (vocab < 4 || vocab > kMaxVocab || vocab % 4)
-    return fail(NSD_ERR_UNSUPPORTED, "spec_accept: vocab must be a multiple of 4 in [4, %d] "
-                "(got %d)", kMaxVocab, vocab);
-  if (max_k < 0 || max_k > kMaxK)
-    return fail(NSD_ERR_UNSUPPORTED, "spec_accept: max_k must be in [0, %d] (got %d)", kMaxK, max_k);
-  if (bs == 0) return NSD_OK;
-  if (!p_target || !uniforms || !q_indptr || !accepted_len || !out_tokens ||
-      (max_k > 0 && (!q_draft || !draft_tokens)))
-    return fail(NSD_ERR_NULL, "spec_accept: NULL pointer argument");
-  if (((uintptr_t)p_target | (uintptr_t)(max_k > 0 ? q_draft : p_target)) & 15)
-    return fail(NSD_ERR_SHAPE, "spec_accept: probability rows must be 16-byte aligned");
-  Args A{p_target, q_draft, draft_tokens, uniforms, q_indptr, bs, vocab, max_k, 0,
-         (int64_t)vocab, 1, nullptr, nullptr, accepted_len, out_tokens};
-  return launch(false, A, bs, workspace, workspace_bytes, stream, "spec_accept");
+  return spec_accept_impl("spec_accept", p_target, q_draft, draft_tokens, uniforms, q_indptr, bs,
+                          vocab, max_k, accepted_len, out_tokens, workspace, workspace_bytes,
+                          stream);
 }
 
 extern "C" nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* uniforms,

@@ -152,10 +152,11 @@ def test_round_with_window_append(device, fused):
     torch.cuda.synchronize()
     from parity import check_attention
     check_attention(meta, lay, outs[0], range(meta.bs))
-    a = make_accept(cfg, meta, "cpu")
-    n_ref, _ = oracle.accept.spec_accept(a.p_target.numpy(), a.q_draft.numpy(),
-                                         a.draft_tokens.numpy(), a.uniforms.numpy(),
-                                         meta.q_indptr)
+    # the generator's inputs (drawn on the device), copied to the host
+    n_ref, _ = oracle.accept.spec_accept(acc_in.p_target.cpu().numpy(),
+                                         acc_in.q_draft.cpu().numpy(),
+                                         acc_in.draft_tokens.cpu().numpy(),
+                                         acc_in.uniforms.cpu().numpy(), meta.q_indptr)
     ref = oracle.commit.commit_lengths(meta.seq_lens, meta.q_indptr, n_ref)
     assert np.array_equal(acc.cpu().numpy(), n_ref)
     assert np.array_equal(committed.cpu().numpy(), ref)
