@@ -344,6 +344,26 @@ nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
                            size_t workspace_bytes, void* stream);
 
 /*
+ * nsd_spec_accept without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, semantics and results
+ * as nsd_spec_accept; its per-chunk sums live in a static device array of
+ * nsd_spec_accept_static_max_bytes() bytes (8 MiB) that each GPU the library
+ * runs on holds until the process ends.  A batch whose
+ * nsd_spec_accept_workspace_size(bs, vocab) exceeds that returns
+ * NSD_ERR_WORKSPACE (e.g. more than 1700 requests at vocab 151936).  The call
+ * allocates nothing.  Every call on one GPU shares that GPU's array: calls
+ * that overlap in time on one GPU race, so order them on one stream.  The
+ * array needs no clearing (each call writes what it reads).
+ */
+size_t     nsd_spec_accept_static_max_bytes(void);
+nsd_status nsd_spec_accept_static(const float* p_target, const float* q_draft,
+                                  const int32_t* draft_tokens, const float* uniforms,
+                                  const int32_t* q_indptr, int32_t bs, int32_t vocab,
+                                  int32_t max_k, int32_t* accepted_len, int32_t* out_tokens,
+                                  void* stream);
+
+/*
  * Draw one token per row by inverse CDF: the sampling of a draft step,
  * x_i ~ q_i (the draft stage precedes verification, Eq. 1; speculative
  * decoding as in the works cited in Sections 1 and 2).

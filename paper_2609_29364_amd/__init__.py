@@ -51,6 +51,8 @@ _SIGS = {
                              _P]),
     "nsd_commit_lengths": (_I32, [_P, _P, _P, _P, _I32, _P]),
     "nsd_host_alias": (_I32, [_P, ctypes.POINTER(ctypes.c_void_p)]),
+    "nsd_spec_accept_static": (_I32, [_P, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]),
+    "nsd_spec_accept_static_max_bytes": (_SZ, []),
     "nsd_set_attention_waves": (_I32, [_I32]),
     "nsd_attention_waves": (_I32, []),
     "nsd_check_plan": (_I32, [_P, _P, _I32, _P, _P, _I32, _I64, _I64, _I32, _I32, _I64]),
@@ -341,6 +343,32 @@ def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, acce
     return accepted_len, out_tokens
 
 
+def spec_accept_static(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k,
+                       accepted_len, out_tokens):
+    """spec_accept through the entry point that allocates nothing (its scratch is a
+    static device array): for callers that cannot allocate, so the outputs are
+    the caller's.  Returns (accepted_len, out_tokens)."""
+    _dev(p_target, torch.float32, "p_target")
+    _dev(uniforms, torch.float32, "uniforms")
+    _dev(q_indptr, torch.int32, "q_indptr")
+    _dev(accepted_len, torch.int32, "accepted_len")
+    _dev(out_tokens, torch.int32, "out_tokens")
+    if max_k > 0:
+        _dev(q_draft, torch.float32, "q_draft")
+        _dev(draft_tokens, torch.int32, "draft_tokens")
+    total_q, vocab = p_target.shape
+    bs = q_indptr.numel() - 1
+    if uniforms.numel() != total_q or out_tokens.numel() != total_q or accepted_len.numel() != bs:
+        raise ValueError("uniforms / out_tokens / accepted_len do not match the rows")
+    if max_k > 0 and (q_draft.shape != (total_q - bs, vocab) or draft_tokens.numel() != total_q - bs):
+        raise ValueError("q_draft / draft_tokens must have total_q - bs rows")
+    _check("spec_accept_static", lib().nsd_spec_accept_static(
+        _ptr(p_target), _ptr(q_draft) if max_k > 0 else None,
+        _ptr(draft_tokens) if max_k > 0 else None, _ptr(uniforms), _ptr(q_indptr), bs, vocab,
+        max_k, _ptr(accepted_len), _ptr(out_tokens), _stream(p_target)))
+    return accepted_len, out_tokens
+
+
 def sample(probs, uniforms, out=None, workspace=None):
     """One token per row by inverse CDF (the draft step's x_i ~ q_i).
 
@@ -450,4 +478,4 @@ def kv_writeback(k_pool, v_pool, host_k, host_v, src_ids, dst_ids):
 __all__ = ["lib", "version", "attention_waves", "check_plan", "check_pairs", "kv_gather", "verify_attention", "verify_attention_workspace_size",
            "new_workspace", "gather_verify_attention", "copy_plan", "COPY_H2D", "COPY_D2H",
            "DEFAULT_CHUNK", "kv_append", "commit_lengths", "host_alias", "kv_writeback",
-           "spec_accept", "accept_workspace_size", "sample", "NsdError", "BLOCK_SIZE", "LIB_PATH"]
+           "spec_accept", "spec_accept_static", "accept_workspace_size", "sample", "NsdError", "BLOCK_SIZE", "LIB_PATH"]

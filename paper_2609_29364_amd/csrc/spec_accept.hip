@@ -29,6 +29,8 @@
 // one 1 KiB chunk per row.
 #include "nsd_internal.h"
 
+#include <mutex>
+
 namespace {
 
 typedef __attribute__((ext_vector_type(4))) float f32x4;
@@ -516,7 +518,7 @@ extern "C" size_t nsd_spec_accept_workspace_size(int32_t rows, int32_t vocab) {
   return (size_t)(sums_bytes(rows, vocab) + (int64_t)rows * 4);
 }
 
-// Validation and launch of nsd_spec_accept.
+// Validation and launch shared by nsd_spec_accept and nsd_spec_accept_static.
 static nsd_status spec_accept_impl(const char* fn, const float* p_target, const float* q_draft,
                             const int32_t* draft_tokens, const float* uniforms,
                             const int32_t* q_indptr, int32_t bs, int32_t vocab, int32_t max_k,
@@ -541,6 +543,42 @@ static nsd_status spec_accept_impl(const char* fn, const float* p_target, const 
   return launch(false, A, bs, workspace, workspace_bytes, stream, fn);
 }
 
+// The workspace of nsd_spec_accept_static: a static device array, one copy
+// per GPU the library runs on, held until the process ends.  Its host-side
+// name is not a device address; kernels get the address hipGetSymbolAddress
+// returns for the current device, looked up once per device and kept.
+static constexpr size_t kScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+static constexpr int kMaxScratchDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxScratchDevices];
+
+static nsd_status scratch_address(void** out) {
+  using namespace nsd;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(NSD_ERR_HIP, "spec_accept_static: no current HIP device");
+  }
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(NSD_ERR_UNSUPPORTED, "spec_accept_static: device %d beyond %d", dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(NSD_ERR_HIP, "spec_accept_static: the scratch array's address: %s",
+                  hipGetErrorString(e));
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return NSD_OK;
+}
+
 extern "C" nsd_status nsd_spec_accept(const float* p_target, const float* q_draft,
                                       const int32_t* draft_tokens, const float* uniforms,
                                       const int32_t* q_indptr, int32_t bs, int32_t vocab,
@@ -550,6 +588,29 @@ extern "C" nsd_status nsd_spec_accept(const float* p_target, const float* q_draf
   return spec_accept_impl("spec_accept", p_target, q_draft, draft_tokens, uniforms, q_indptr, bs,
                           vocab, max_k, accepted_len, out_tokens, workspace, workspace_bytes,
                           stream);
+}
+
+extern "C" size_t nsd_spec_accept_static_max_bytes(void) { return kScratchBytes; }
+
+extern "C" nsd_status nsd_spec_accept_static(const float* p_target, const float* q_draft,
+                                             const int32_t* draft_tokens, const float* uniforms,
+                                             const int32_t* q_indptr, int32_t bs, int32_t vocab,
+                                             int32_t max_k, int32_t* accepted_len,
+                                             int32_t* out_tokens, void* stream) {
+  using namespace nsd;
+  const char* fn = "spec_accept_static";
+  if (bs > 0 && vocab >= 4 && vocab <= kMaxVocab &&
+      nsd_spec_accept_workspace_size(bs, vocab) > kScratchBytes)
+    return fail(NSD_ERR_WORKSPACE, "%s: bs %d at vocab %d needs %zu bytes of scratch, more "
+                "than its %zu", fn, bs, vocab, nsd_spec_accept_workspace_size(bs, vocab),
+                kScratchBytes);
+  void* ws = nullptr;
+  if (bs > 0) {
+    const nsd_status st = scratch_address(&ws);
+    if (st != NSD_OK) return st;
+  }
+  return spec_accept_impl(fn, p_target, q_draft, draft_tokens, uniforms, q_indptr, bs, vocab,
+                          max_k, accepted_len, out_tokens, ws, kScratchBytes, stream);
 }
 
 extern "C" nsd_status nsd_sample(const float* probs, int64_t row_stride, const float* uniforms,
