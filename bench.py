@@ -493,8 +493,148 @@ def h2d_bench(args):
                             "t_overlap_ms": None if t_overlap is None else round(t_overlap, 4),
                             "rounds_inside_copy": len(inside),
                             "delta_t": None if t_overlap is None else round((t_overlap - t_base) / t_base, 4)},
-           "pipeline": pipeline, "close": close}
+           "pipeline": pipeline, "close": close,
+           "bounded_submission": bounded_submission(args, nsd, torch, meta, layer, host, bank, bb,
+                                                    plan_all, round_, comp, bt, sl, qi, acc_len,
+                                                    wsrc, wdst)}
     print(json.dumps(res), flush=True)
+
+
+def bounded_submission(args, nsd, torch, meta, layer, host, bank, bb, plan_all, round_, comp,
+                       bt, sl, qi, acc_len, wsrc, wdst):
+    """Bounded H2D submission (Appendix E.5) and the export step of the bank
+    lifecycle (Eq. E.2/E.3), measured on one GPU.
+
+    * head-of-line: while the whole arriving KV of a round (both planes) is
+      restored into one bank by H2D copies -- all 32 MiB chunks queued at
+      once, or submitted by a DMA thread that keeps at most a 32 or 64 MiB
+      window in flight -- the other bank's writeback (the round's committed
+      suffix, by SDMA D2H copies into the pinned arena) is submitted 1 ms later
+      on its own stream: its latency from submission to completion, against the
+      same writeback alone.
+    * rounds with exports: double-banked rounds where round k+1's H2D and round
+      k's export both overlap computation (Compute_k || H2D_k+1, Compute_k+1 ||
+      D2H_k), with and without the window: rounds/s, exposed KV-ready wait
+      (Eq. G.1) and the round time against rounds with no transfer (Eq. D.1)."""
+    import threading
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    d2h = bank.d2h_stream
+    block = bb
+    # the writeback as SDMA copies: pool block -> arena block, both planes
+    wb_k = np.stack([wsrc.astype(np.int64) * block, wdst.astype(np.int64) * block,
+                     np.full(len(wsrc), block, np.int64)], axis=1)
+
+    def writeback_sdma(stream):
+        nsd.copy_plan(layer.k_pool, host.k, wb_k, stream=stream)
+        nsd.copy_plan(layer.v_pool, host.v, wb_k, stream=stream)
+
+    wsrc_d = torch.as_tensor(wsrc, dtype=torch.int32, device=comp.device)
+    wdst_d = torch.as_tensor(wdst, dtype=torch.int32, device=comp.device)
+
+    def writeback_kernel(stream):
+        nsd.kv_writeback(layer.k_pool, layer.v_pool, host.k, host.v, wsrc_d, wdst_d)
+
+    def wb_latency_ms():
+        t0 = time.perf_counter()
+        writeback_sdma(d2h)
+        e = ev(); e.record(d2h)
+        e.synchronize()
+        return (time.perf_counter() - t0) * 1e3
+
+    torch.cuda.synchronize()
+    alone = float(np.median([wb_latency_ms() for _ in range(5)]))
+    hol = {"writeback_bytes": 2 * int(wb_k[:, 2].sum()), "writeback_alone_ms": round(alone, 3)}
+    windows = (("all_queued", None), ("window_32MiB", nsd.DEFAULT_CHUNK),
+               ("window_64MiB", 2 * nsd.DEFAULT_CHUNK))
+    for name, window in windows:
+        lat, h2d_ms = [], []
+        for _ in range(3):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            bank.prepare(1, host.k, host.v, plan_all, plan_all, window_bytes=window)
+            time.sleep(1e-3)
+            lat.append(wb_latency_ms())
+            e = bank.ready(1)
+            e.synchronize()
+            h2d_ms.append((time.perf_counter() - t0) * 1e3)
+        hol[name] = {"writeback_ms": round(float(np.median(lat)), 3),
+                     "h2d_ms": round(float(np.median(h2d_ms)), 3)}
+
+    # double-banked rounds with the export of each round's suffix
+    def run_rounds(n, window, export):
+        torch.cuda.synchronize()
+        t0 = ev(); t0.record(comp)
+        bank.copy_stream.wait_event(t0)
+        h_ev, r_ev = [], []
+        bank.prepare(0, host.k, host.v, plan_all, plan_all, window_bytes=window)
+        for i in range(n):
+            if i + 1 < n:
+                bank.prepare(i + 1, host.k, host.v, plan_all, plan_all, window_bytes=window)
+            bank.computing(i, comp)
+            h_ev.append(bank.ready(i))
+            round_(i)
+            e = ev(); e.record(comp); r_ev.append(e)
+            if export:
+                bank.export(i, comp, export)
+            else:
+                bank.done(i, comp)
+        torch.cuda.synchronize()
+        H = [t0.elapsed_time(x) for x in h_ev]
+        R = [t0.elapsed_time(x) for x in r_ev]
+        W = [0.0] + R[:-1]
+        E = [max(0.0, H[i] - W[i]) for i in range(n)]
+        return {"rounds_per_s": round((n - 1) / ((R[-1] - R[0]) * 1e-3), 1),
+                "exposed_wait_ms_mean": round(float(np.mean(E[1:])), 4)}
+
+    rounds = {"export": "the round's committed suffix written back into the pinned arena by "
+                        "the gather kernel through the arena's device alias, on the D2H stream"}
+    for name, window in windows:
+        rounds[name] = run_rounds(8, window, writeback_kernel)
+    rounds["all_queued_no_export"] = run_rounds(8, None, None)
+
+    # Eq. D.1 for the round while both an H2D and an export run: the export by
+    # SDMA copies, or by the writeback kernel (which takes compute units)
+    def timed(n):
+        e = [ev() for _ in range(n + 1)]
+        e[0].record(comp)
+        for k in range(n):
+            round_(0)
+            e[k + 1].record(comp)
+        return e
+    torch.cuda.synchronize()
+    eb = timed(args.steps)
+    torch.cuda.synchronize()
+    t_base = eb[0].elapsed_time(eb[-1]) / args.steps
+    interference = {"t_base_ms": round(t_base, 4)}
+    for kind, fn in (("sdma_export", writeback_sdma), ("kernel_export", writeback_kernel)):
+        torch.cuda.synchronize()
+        s0 = ev(); s0.record(bank.copy_stream)
+        bank.prepare(1, host.k, host.v, plan_all, plan_all)
+        stop = threading.Event()
+
+        def exporter(fn=fn):
+            torch.cuda.set_device(comp.device)
+            while not stop.is_set():
+                with torch.cuda.stream(d2h):
+                    fn(d2h)
+                e = ev(); e.record(d2h); e.synchronize()
+        th = threading.Thread(target=exporter, daemon=True)
+        th.start()
+        n_ov = 8
+        eo = timed(n_ov)
+        e_h2d = bank.ready(1)
+        torch.cuda.synchronize()
+        stop.set()
+        th.join()
+        ends = [s0.elapsed_time(x) for x in eo]
+        h_end = s0.elapsed_time(e_h2d)
+        inside = [k for k in range(n_ov) if ends[k + 1] <= h_end]
+        t_ov = float(np.mean([ends[k + 1] - ends[k] for k in inside])) if inside else None
+        interference[kind] = {"t_overlap_ms": None if t_ov is None else round(t_ov, 4),
+                              "rounds_inside_copy": len(inside),
+                              "delta_t": None if t_ov is None else round((t_ov - t_base) / t_base, 4)}
+    return {"head_of_line": hol, "rounds_with_export": rounds,
+            "interference_h2d_and_export": interference}
 
 
 def draft_bench(args):
@@ -1038,17 +1178,19 @@ def main():
     parts = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
                       for e in evs])
     g_ms, a_ms, c_ms = parts.mean(0)
-    # per-step spread, and the same steps after an untimed 1 GiB write that
-    # evicts the 256 MB last-level cache (MALL) before each step: the A/B shows
-    # how much of the back-to-back figure any cache carry-over could explain
-    scrub = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    # per-step spread, and the same steps after an untimed 1 GiB read that
+    # evicts the 256 MB last-level cache (MALL) before each step (a read, so
+    # the scrub leaves no dirty lines to be written back during the step): the
+    # A/B shows how much of the back-to-back figure any cache carry-over explains
+    scrub = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    scrub_sink = torch.empty((), dtype=torch.float32, device=dev)
 
     def per_step(scrubbed):
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(args.steps)]
         for i in range(args.steps):
             if scrubbed:
-                scrub.fill_(i & 0xFF)
+                torch.sum(scrub, dim=0, out=scrub_sink)
             ev[i][0].record(stream)
             step()
             ev[i][1].record(stream)
@@ -1056,13 +1198,13 @@ def main():
         return np.array([a.elapsed_time(b) for a, b in ev])
 
     t_plain, t_scrub = per_step(False), per_step(True)
-    del scrub
+    del scrub, scrub_sink
     spread = {"median": round(float(np.median(t_plain)), 5),
               "min": round(float(t_plain.min()), 5), "max": round(float(t_plain.max()), 5),
               "median_scrubbed": round(float(np.median(t_scrub)), 5),
               "min_scrubbed": round(float(t_scrub.min()), 5),
               "max_scrubbed": round(float(t_scrub.max()), 5),
-              "scrub_bytes": 1 << 30,
+              "scrub_bytes_read": 1 << 30,
               "scrub_effect": round(float(np.median(t_scrub) / np.median(t_plain) - 1.0), 4)}
     acc_host = acc_len.cpu().numpy() if acc_in is not None else None
     alg = algorithmic_bytes(cfg, meta, acc_host)

@@ -247,6 +247,64 @@ nsd_status nsd_copy_plan(const void* src, int64_t src_bytes, void* dst, int64_t 
                          int32_t direction, void* stream);
 
 /*
+ * nsd_copy_plan with bounded submission (Appendix E.5: only a bounded group
+ * of chunks of a large H2D plan is submitted before the DMA process waits for
+ * its completion and submits the next group, so one bank's restore cannot
+ * queue far ahead of the other bank's writeback on the shared copy path).
+ * Chunks of at most chunk_bytes are submitted so that at most window_bytes
+ * (>= 1; a chunk larger than the window goes alone) and at most 64 chunks of
+ * this plan are in flight: before submitting a chunk that would exceed that,
+ * the call waits, on the calling host thread, until the oldest chunks in
+ * flight have completed.  It returns once the last chunk is submitted (its
+ * copies still run); callers run it on a DMA thread of their own.  Other
+ * arguments, checks and errors as nsd_copy_plan.
+ */
+nsd_status nsd_copy_plan_windowed(const void* src, int64_t src_bytes, void* dst,
+                                  int64_t dst_bytes, const int64_t* copies, int64_t n_copies,
+                                  int64_t chunk_bytes, int64_t window_bytes, int32_t direction,
+                                  void* stream);
+
+/*
+ * The preparation's copy plan (host code): block j < ceil(seq_lens[r] / 16)
+ * of every arriving request r (arriving[r] != 0) goes from arena block
+ * extent[r] + j to bank block stage_table[r][j], as the triple
+ * (arena byte offset, bank byte offset, block_bytes), request by request.
+ *
+ * Passage: Algorithm 1 (Prepare restores the batch's state on the worker);
+ * Appendix E.1 (stable per-request extents in the host arena, Eq. E.1);
+ * Appendix E.4 (copy plans as compact descriptors).
+ * extent: int64 [bs]; stage_table: int32 [bs][max_blocks_per_seq];
+ * arriving: uint8 [bs]; seq_lens: int32 [bs]; copies: int64 [capacity][3].
+ * *n_copies gets the plan's length; if it exceeds capacity only the first
+ * capacity triples are written and NSD_ERR_WORKSPACE is returned.  A request
+ * with more blocks than the table holds returns NSD_ERR_SHAPE.  Host memory.
+ */
+nsd_status nsd_h2d_plan(const int64_t* extent, const int32_t* stage_table,
+                        int32_t max_blocks_per_seq, const uint8_t* arriving,
+                        const int32_t* seq_lens, int32_t bs, int64_t block_bytes,
+                        int64_t* copies, int64_t capacity, int64_t* n_copies);
+
+/*
+ * The writeback's block pairs (host code): with host_len[r] tokens already in
+ * the arena and new_len[r] committed, the blocks holding tokens host_len[r] ..
+ * new_len[r] - 1 go from pool block block_table[r][j] to arena block
+ * extent[r] + j, request by request (nsd_kv_gather's (src, dst) pairs, e.g.
+ * through nsd_host_alias).
+ *
+ * Passage: Section 5 (incremental writeback of only the valid suffix not yet
+ * persistent); Appendix E.1 (stable extents); Appendix E.2 (a bank exports its
+ * updated suffix before it is released).
+ * block_table: int32 [bs][max_blocks_per_seq]; extent: int64 [bs]; host_len,
+ * new_len: int32 [bs]; src_ids, dst_ids: int32 [capacity].  *n_pairs and
+ * NSD_ERR_WORKSPACE as nsd_h2d_plan; tokens outside the table or an arena
+ * block beyond 2^31 - 1 return an error.  Host memory.
+ */
+nsd_status nsd_writeback_pairs(const int32_t* block_table, int32_t max_blocks_per_seq,
+                               const int64_t* extent, const int32_t* host_len,
+                               const int32_t* new_len, int32_t bs, int32_t* src_ids,
+                               int32_t* dst_ids, int64_t capacity, int64_t* n_pairs);
+
+/*
  * Append the window's new K/V rows to the paged cache, for one layer.
  *
  * Passage: Section 3 (the cache is paged and append-dominant: an iteration

@@ -47,6 +47,9 @@ _SIGS = {
                                ctypes.c_double, ctypes.c_double, _P, _P, _P]),
     "nsd_simulate": (_I32, [_P, _P, _I32, _P, _I32, _P, _P, _I64, _P, _I64, _P, _P]),
     "nsd_copy_plan": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I32, _P]),
+    "nsd_copy_plan_windowed": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I32, _P]),
+    "nsd_h2d_plan": (_I32, [_P, _P, _I32, _P, _P, _I32, _I64, _P, _I64, _P]),
+    "nsd_writeback_pairs": (_I32, [_P, _I32, _P, _P, _P, _I32, _P, _P, _I64, _P]),
     "nsd_kv_append": (_I32, [_P, _P, _I64, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _I32, _I32,
                              _P]),
     "nsd_commit_lengths": (_I32, [_P, _P, _P, _P, _I32, _P]),
@@ -401,12 +404,14 @@ COPY_H2D, COPY_D2H = 1, 2
 DEFAULT_CHUNK = 32 << 20   # bytes per DMA submission
 
 
-def copy_plan(src, dst, copies, chunk_bytes=DEFAULT_CHUNK, stream=None):
+def copy_plan(src, dst, copies, chunk_bytes=DEFAULT_CHUNK, stream=None, window_bytes=None):
     """Execute a KV copy plan between a pinned host tensor and a device tensor.
 
     copies: int64 array [n][3] of (source byte offset, destination byte offset,
     bytes).  The direction follows the tensors' devices; the host tensor must be
-    pinned.  Runs on ``stream`` (a torch.cuda.Stream) or the current stream."""
+    pinned.  Runs on ``stream`` (a torch.cuda.Stream) or the current stream.
+    With ``window_bytes`` the chunks are submitted in bounded groups and the
+    call blocks until the last group is submitted (nsd_copy_plan_windowed)."""
     import numpy as np
     if src.is_cuda == dst.is_cuda:
         raise ValueError("copy_plan moves between a pinned host tensor and a device tensor")
@@ -417,10 +422,17 @@ def copy_plan(src, dst, copies, chunk_bytes=DEFAULT_CHUNK, stream=None):
         raise ValueError("src and dst must be contiguous")
     plan = np.ascontiguousarray(np.asarray(copies, dtype=np.int64).reshape(-1, 3))
     st = (stream or torch.cuda.current_stream(dev.device)).cuda_stream
-    _check("copy_plan", lib().nsd_copy_plan(
-        _ptr(src), src.numel() * src.element_size(), _ptr(dst), dst.numel() * dst.element_size(),
-        plan.ctypes.data if len(plan) else None, len(plan), int(chunk_bytes),
-        COPY_H2D if dst.is_cuda else COPY_D2H, st))
+    direction = COPY_H2D if dst.is_cuda else COPY_D2H
+    if window_bytes is None:
+        _check("copy_plan", lib().nsd_copy_plan(
+            _ptr(src), src.numel() * src.element_size(), _ptr(dst),
+            dst.numel() * dst.element_size(), plan.ctypes.data if len(plan) else None,
+            len(plan), int(chunk_bytes), direction, st))
+    else:
+        _check("copy_plan_windowed", lib().nsd_copy_plan_windowed(
+            _ptr(src), src.numel() * src.element_size(), _ptr(dst),
+            dst.numel() * dst.element_size(), plan.ctypes.data if len(plan) else None,
+            len(plan), int(chunk_bytes), int(window_bytes), direction, st))
 
 
 def kv_append(k_pool, v_pool, k_new, v_new, block_table, seq_lens, q_indptr):

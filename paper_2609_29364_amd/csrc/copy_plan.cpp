@@ -12,6 +12,10 @@
 // run is issued as asynchronous copies of at most chunk_bytes on the caller's
 // stream (the caller uses a stream of its own for background preparation).
 // No kernel runs: the copies use the SDMA engines, not the compute units.
+// The windowed variant is the bounded submission of Appendix E.5: only a
+// group of chunks up to window_bytes is queued at a time, and the calling
+// (DMA) thread waits for each group to complete before it submits the next,
+// so a large restore cannot queue far ahead of the other bank's writeback.
 #include "nsd_internal.h"
 
 namespace {
@@ -34,13 +38,18 @@ bool device_mem(const void* p) {
   return a.type == hipMemoryTypeDevice;
 }
 
-}  // namespace
-
-extern "C" nsd_status nsd_copy_plan(const void* src, int64_t src_bytes, void* dst,
-                                    int64_t dst_bytes, const int64_t* copies, int64_t n_copies,
-                                    int64_t chunk_bytes, int32_t direction, void* stream) {
+// Validation and submission shared by both entry points.  window_bytes > 0
+// bounds the bytes submitted ahead of completion: before a chunk that would
+// take the bytes in flight past the window is submitted, the calling thread
+// waits until the oldest chunks in flight have completed (an event recorded
+// after each chunk, kept in a ring), so the copy path holds at most a window
+// of this plan at any time while the next chunk is already queued behind the
+// one running.
+nsd_status submit_plan(const char* fn, const void* src, int64_t src_bytes, void* dst,
+                       int64_t dst_bytes, const int64_t* copies, int64_t n_copies,
+                       int64_t chunk_bytes, int64_t window_bytes, int32_t direction,
+                       void* stream) {
   using namespace nsd;
-  const char* fn = "copy_plan";
   if (n_copies < 0) return fail(NSD_ERR_SHAPE, "%s: n_copies < 0", fn);
   if (direction != NSD_COPY_H2D && direction != NSD_COPY_D2H)
     return fail(NSD_ERR_SHAPE, "%s: direction must be NSD_COPY_H2D or NSD_COPY_D2H", fn);
@@ -67,6 +76,25 @@ extern "C" nsd_status nsd_copy_plan(const void* src, int64_t src_bytes, void* ds
   const char* s8 = (const char*)src;
   char* d8 = (char*)dst;
   clear_stale_error();
+  // ring of the chunks in flight: completion event and bytes, oldest first
+  constexpr int kRing = 64;
+  hipEvent_t ring[kRing] = {};
+  int64_t ring_bytes[kRing] = {};
+  int head = 0, count = 0;
+  int64_t in_flight = 0;
+  auto finish = [&](nsd_status st) {
+    for (int k = 0; k < kRing; ++k)
+      if (ring[k]) (void)hipEventDestroy(ring[k]);
+    return st;
+  };
+  if (window_bytes > 0) {
+    for (int k = 0; k < kRing; ++k) {
+      const hipError_t e = hipEventCreateWithFlags(&ring[k], hipEventDisableTiming);
+      if (e != hipSuccess)
+        return finish(fail(NSD_ERR_HIP, "%s: hipEventCreateWithFlags: %s", fn,
+                           hipGetErrorString(e)));
+    }
+  }
   int64_t i = 0;
   while (i < n_copies) {
     // merge the triples that continue this run in both buffers
@@ -78,11 +106,128 @@ extern "C" nsd_status nsd_copy_plan(const void* src, int64_t src_bytes, void* ds
     }
     for (int64_t o = 0; o < b; o += chunk_bytes) {
       const int64_t len = b - o < chunk_bytes ? b - o : chunk_bytes;
-      const hipError_t e = hipMemcpyAsync(d8 + d + o, s8 + s + o, (size_t)len, kind,
-                                          (hipStream_t)stream);
+      // wait for the oldest chunks until this one fits in the window (and
+      // the ring has a free entry)
+      while (window_bytes > 0 && count > 0 &&
+             (in_flight + len > window_bytes || count == kRing)) {
+        const hipError_t e = hipEventSynchronize(ring[head]);
+        if (e != hipSuccess)
+          return finish(fail(NSD_ERR_HIP, "%s: waiting for a chunk: %s", fn,
+                             hipGetErrorString(e)));
+        in_flight -= ring_bytes[head];
+        head = (head + 1) % kRing;
+        --count;
+      }
+      hipError_t e = hipMemcpyAsync(d8 + d + o, s8 + s + o, (size_t)len, kind,
+                                    (hipStream_t)stream);
       if (e != hipSuccess)
-        return fail(NSD_ERR_HIP, "%s: hipMemcpyAsync: %s", fn, hipGetErrorString(e));
+        return finish(fail(NSD_ERR_HIP, "%s: hipMemcpyAsync: %s", fn, hipGetErrorString(e)));
+      if (window_bytes > 0) {
+        const int k = (head + count) % kRing;
+        e = hipEventRecord(ring[k], (hipStream_t)stream);
+        if (e != hipSuccess)
+          return finish(fail(NSD_ERR_HIP, "%s: hipEventRecord: %s", fn, hipGetErrorString(e)));
+        ring_bytes[k] = len;
+        in_flight += len;
+        ++count;
+      }
     }
   }
+  return finish(NSD_OK);
+}
+
+}  // namespace
+
+extern "C" nsd_status nsd_copy_plan(const void* src, int64_t src_bytes, void* dst,
+                                    int64_t dst_bytes, const int64_t* copies, int64_t n_copies,
+                                    int64_t chunk_bytes, int32_t direction, void* stream) {
+  return submit_plan("copy_plan", src, src_bytes, dst, dst_bytes, copies, n_copies, chunk_bytes,
+                     0, direction, stream);
+}
+
+extern "C" nsd_status nsd_copy_plan_windowed(const void* src, int64_t src_bytes, void* dst,
+                                             int64_t dst_bytes, const int64_t* copies,
+                                             int64_t n_copies, int64_t chunk_bytes,
+                                             int64_t window_bytes, int32_t direction,
+                                             void* stream) {
+  if (window_bytes < 1)
+    return nsd::fail(NSD_ERR_SHAPE, "copy_plan_windowed: window_bytes < 1");
+  return submit_plan("copy_plan_windowed", src, src_bytes, dst, dst_bytes, copies, n_copies,
+                     chunk_bytes, window_bytes, direction, stream);
+}
+
+// Plan arithmetic of the preparation and the writeback (host code).
+//
+// H2D plan (Algorithm 1, Prepare; Appendix E.1, Eq. E.1): block j of
+// arriving request r goes from arena block extent[r] + j to bank block
+// stage_table[r][j], for j < ceil(seq_lens[r] / 16), request by request (a
+// request whose staging ids are consecutive becomes one run once merged).
+extern "C" nsd_status nsd_h2d_plan(const int64_t* extent, const int32_t* stage_table,
+                                   int32_t max_blocks_per_seq, const uint8_t* arriving,
+                                   const int32_t* seq_lens, int32_t bs, int64_t block_bytes,
+                                   int64_t* copies, int64_t capacity, int64_t* n_copies) {
+  using namespace nsd;
+  const char* fn = "h2d_plan";
+  if (bs < 0 || max_blocks_per_seq < 1 || block_bytes < 1 || capacity < 0)
+    return fail(NSD_ERR_SHAPE, "%s: bad sizes", fn);
+  if (!n_copies) return fail(NSD_ERR_NULL, "%s: NULL pointer argument", fn);
+  if (bs > 0 && (!extent || !stage_table || !arriving || !seq_lens))
+    return fail(NSD_ERR_NULL, "%s: NULL pointer argument", fn);
+  int64_t n = 0;
+  for (int32_t r = 0; r < bs; ++r) {
+    if (!arriving[r]) continue;
+    const int64_t nb = seq_lens[r] > 0 ? ((int64_t)seq_lens[r] + NSD_BLOCK_SIZE - 1) / NSD_BLOCK_SIZE
+                                       : 0;
+    if (nb > max_blocks_per_seq)
+      return fail(NSD_ERR_SHAPE, "%s: request %d has %lld blocks, more than the table's %d", fn,
+                  r, (long long)nb, max_blocks_per_seq);
+    for (int64_t j = 0; j < nb; ++j, ++n) {
+      if (n >= capacity || !copies) continue;   // counted, not written
+      copies[3 * n] = (extent[r] + j) * block_bytes;
+      copies[3 * n + 1] = (int64_t)stage_table[(int64_t)r * max_blocks_per_seq + j] * block_bytes;
+      copies[3 * n + 2] = block_bytes;
+    }
+  }
+  *n_copies = n;
+  if (n > capacity) return fail(NSD_ERR_WORKSPACE, "%s: %lld copies, room for %lld", fn,
+                                (long long)n, (long long)capacity);
+  return NSD_OK;
+}
+
+// Writeback pairs (Section 5: incremental writeback of the valid suffix;
+// Appendix E.1 extents): with host_len[r] tokens already in the arena and
+// new_len[r] committed, the blocks holding tokens host_len .. new_len - 1 go
+// from pool block block_table[r][j] to arena block extent[r] + j, request by
+// request.
+extern "C" nsd_status nsd_writeback_pairs(const int32_t* block_table, int32_t max_blocks_per_seq,
+                                          const int64_t* extent, const int32_t* host_len,
+                                          const int32_t* new_len, int32_t bs, int32_t* src_ids,
+                                          int32_t* dst_ids, int64_t capacity, int64_t* n_pairs) {
+  using namespace nsd;
+  const char* fn = "writeback_pairs";
+  if (bs < 0 || max_blocks_per_seq < 1 || capacity < 0)
+    return fail(NSD_ERR_SHAPE, "%s: bad sizes", fn);
+  if (!n_pairs) return fail(NSD_ERR_NULL, "%s: NULL pointer argument", fn);
+  if (bs > 0 && (!block_table || !extent || !host_len || !new_len))
+    return fail(NSD_ERR_NULL, "%s: NULL pointer argument", fn);
+  int64_t n = 0;
+  for (int32_t r = 0; r < bs; ++r) {
+    const int64_t h = host_len[r], l = new_len[r];
+    if (l <= h) continue;
+    if (h < 0 || (l - 1) / NSD_BLOCK_SIZE >= max_blocks_per_seq)
+      return fail(NSD_ERR_SHAPE, "%s: request %d: tokens [%lld, %lld) outside its block table", fn,
+                  r, (long long)h, (long long)l);
+    for (int64_t j = h / NSD_BLOCK_SIZE; j <= (l - 1) / NSD_BLOCK_SIZE; ++j, ++n) {
+      if (n >= capacity || !src_ids || !dst_ids) continue;
+      const int64_t a = extent[r] + j;
+      if (a > INT32_MAX)
+        return fail(NSD_ERR_UNSUPPORTED, "%s: arena block %lld beyond 2^31 - 1", fn, (long long)a);
+      src_ids[n] = block_table[(int64_t)r * max_blocks_per_seq + j];
+      dst_ids[n] = (int32_t)a;
+    }
+  }
+  *n_pairs = n;
+  if (n > capacity) return fail(NSD_ERR_WORKSPACE, "%s: %lld pairs, room for %lld", fn,
+                                (long long)n, (long long)capacity);
   return NSD_OK;
 }

@@ -270,3 +270,44 @@ def test_check_pairs(lib):
         with pytest.raises(nsd.NsdError) as e:
             nsd.check_pairs(np.array(s), np.array(d), 9, 64)
         assert needle in str(e.value)
+
+
+def test_windowed_copy_and_plan_validation(lib):
+    import numpy as np
+    f = lib.nsd_copy_plan_windowed
+    plan = (ctypes.c_int64 * 3)(0, 0, 64)
+    fake = ctypes.c_void_p(16)  # never dereferenced: every case fails before any copy
+    assert f(fake, 128, fake, 128, plan, 1, 1 << 20, 0, 1, None) == 2       # window < 1
+    assert f(fake, 128, fake, 128, plan, 1, 0, 1 << 20, 1, None) == 2       # chunk < 1
+    assert f(None, 0, None, 0, None, 0, 1 << 20, 1 << 20, 1, None) == 0     # empty plan
+    # h2d plan: capacity too small reports the length needed
+    n = ctypes.c_int64()
+    ext = np.array([0, 10], np.int64)
+    st = np.array([[3, 4, -1], [5, 6, 7]], np.int32)
+    arr = np.array([1, 1], np.uint8)
+    sl = np.array([20, 40], np.int32)
+    out = np.zeros((8, 3), np.int64)
+    h = lib.nsd_h2d_plan
+    assert h(ext.ctypes.data, st.ctypes.data, 3, arr.ctypes.data, sl.ctypes.data, 2, 100,
+             out.ctypes.data, 2, ctypes.byref(n)) == 4 and n.value == 5
+    assert h(ext.ctypes.data, st.ctypes.data, 3, arr.ctypes.data, sl.ctypes.data, 2, 100,
+             out.ctypes.data, 8, ctypes.byref(n)) == 0 and n.value == 5
+    assert out[:5].tolist() == [[0, 300, 100], [100, 400, 100], [1000, 500, 100],
+                                [1100, 600, 100], [1200, 700, 100]]
+    sl2 = np.array([20, 49], np.int32)       # 4 blocks in a 3-entry table
+    assert h(ext.ctypes.data, st.ctypes.data, 3, arr.ctypes.data, sl2.ctypes.data, 2, 100,
+             out.ctypes.data, 8, ctypes.byref(n)) == 2
+    w = lib.nsd_writeback_pairs
+    bt = np.array([[9, 8, 7], [6, 5, 4]], np.int32)
+    s_ = np.zeros(8, np.int32)
+    d_ = np.zeros(8, np.int32)
+    hl = np.array([15, 16], np.int32)
+    nl = np.array([17, 33], np.int32)
+    assert w(bt.ctypes.data, 3, ext.ctypes.data, hl.ctypes.data, nl.ctypes.data, 2,
+             s_.ctypes.data, d_.ctypes.data, 8, ctypes.byref(n)) == 0 and n.value == 4
+    assert s_[:4].tolist() == [9, 8, 5, 4] and d_[:4].tolist() == [0, 1, 11, 12]
+    nl_bad = np.array([17, 49], np.int32)    # past the table
+    assert w(bt.ctypes.data, 3, ext.ctypes.data, hl.ctypes.data, nl_bad.ctypes.data, 2,
+             s_.ctypes.data, d_.ctypes.data, 8, ctypes.byref(n)) == 2
+    assert w(bt.ctypes.data, 3, ext.ctypes.data, hl.ctypes.data, nl.ctypes.data, 2,
+             s_.ctypes.data, d_.ctypes.data, 1, ctypes.byref(n)) == 4 and n.value == 4
