@@ -89,6 +89,23 @@ __host__ __device__ constexpr int span_blocks(int d, int mt, bool fuse) {
   return (fuse && d * mt > 128) ? 2 : (d * mt <= 256 ? 4 : 2);
 }
 
+// Waves per SIMD an instantiation is compiled for, and the most its launch
+// keeps resident: one.  The larger tiles take the whole register file; the
+// single-tile attention without fusion (the decode shape) fits twice, but two
+// waves per SIMD measured no faster (decode attention on the draft_decode
+// shape 489 against 461-470 us: the second wave's K/V stream adds bytes in
+// flight past what HBM rewards).
+__host__ __device__ constexpr int waves_per_simd(int, int, bool) { return 1; }
+
+// The item a range cuts at its end and that began in that range (the one the
+// merge kernel's workgroup for the range finishes), with what the merge needs
+// to find its parts: written by the range's wave when its work ends.
+struct CutRec {
+  int64_t base;     // span position of the item's first span
+  int32_t n;        // the item's spans; -1: the range leaves nothing to merge
+  int32_t r, g, qo, nq, pad;
+};
+
 struct Params {
   const uint16_t* q;
   const uint16_t* k_cache;   // worker pool (read for resident requests)
@@ -104,8 +121,10 @@ struct Params {
   uint16_t* out;
   float* part_o;       // [4 * waves][MT*16][D]: head/tail partial O per range
   float2* part_ml;     // [4 * waves][MT*16]: (running max, sum)
+  struct CutRec* cut_rec;  // [2 * waves]: the item each range cuts at its end, for the merge
   uint32_t* prefix;    // [bs+1]: exclusive span prefix over the work order's positions
-  uint32_t* pos_of;    // [bs+1]: position of each request; [bs]: resident requests
+  uint32_t* pos_of;    // [bs+1]: position of each request; [bs]: resident requests;
+                       // then [2]: spans of the two segments (per KV head)
   int32_t num_blocks;    // blocks in the worker pool (tiles fit 32-bit indexes)
   int32_t stage_blocks;  // blocks in the staging pool (0 without fusion)
   int32_t bs;
@@ -824,6 +843,26 @@ __device__ inline void run_item(const Params& p, const int32_t* __restrict__ blo
                                          p, a, it.win, it.L, total_q, lane);
 }
 
+// The record of range rid for the merge: the item it cuts at its end (if that
+// item began in the range), or none.
+__device__ __attribute__((always_inline)) inline void write_cut_rec(
+    const Params& p, int64_t rid, int lane, bool cut, int64_t base, int n, int r, int g, int qo,
+    int nq) {
+  if (lane != 0) return;
+  CutRec* c = p.cut_rec + rid;
+  c->base = base;
+  c->n = cut ? n : -1;
+  c->r = r;
+  c->g = g;
+  c->qo = qo;
+  c->nq = nq;
+}
+
+__device__ __attribute__((always_inline)) inline void write_no_cut(const Params& p, int64_t rid,
+                                                                    int lane) {
+  write_cut_rec(p, rid, lane, false, 0, 0, 0, 0, 0, 0);
+}
+
 // One range [s, s1) of global spans, range id rid: online softmax over every
 // (request, KV head) item the range touches.
 template <int D, int MT, int NB, bool FUSE>
@@ -843,9 +882,9 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
   Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos0, r0, g0, pr0, s, s1,
                                 total_q);
   if (it.j0 >= it.j1) {
-    if (it.pos == p.bs - 1 && it.g == hkv - 1) return;
+    if (it.pos == p.bs - 1 && it.g == hkv - 1) return write_no_cut(p, rid, lane);
     it = next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, it, s, s1, total_q);
-    if (it.j0 >= it.j1) return;   // no span lies in this range
+    if (it.j0 >= it.j1) return write_no_cut(p, rid, lane);   // no span lies here
   }
   // next item with a span in the range (or `it` itself when none)
   auto following = [&](const Item& cur) {
@@ -879,7 +918,12 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
       run_item<D, MT, NB, FUSE, false>(p, block_table, stage_table, it, next, kreg, vreg, cur,
                                        qc, a, total_q, lane);
     finish_item<D, MT>(p, a, it, rid, lane, ob);
-    if (!more) break;
+    if (!more) {
+      // the range's last item, if it began here and continues past the range
+      const bool cut = it.j0 == 0 && it.j1 < it.n && it.rows > 0;
+      write_cut_rec(p, rid, lane, cut, it.base, it.n, it.r, it.g, it.qo, it.nq);
+      break;
+    }
     // switch to the next item (its first span, and Q without fusion, are
     // already requested)
     if constexpr (FUSE) load_q<D, MT>(qc, p, next, total_q, lane);
@@ -962,7 +1006,7 @@ __device__ void copy_staged(const Params& p, const int32_t* __restrict__ block_t
 // writes spread through a read stream.  Without fusion there is one segment
 // and position i is request i.
 template <int D, int MT, bool FUSE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(waves_per_simd(D, MT, FUSE))))
 void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
                              const int32_t* __restrict__ stage_table,
                              const int32_t* __restrict__ seq_lens,
@@ -1039,6 +1083,8 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
     if (blockIdx.x == 0) {
       p.prefix[p.bs] = c_ua + c_ur;
       p.pos_of[p.bs] = n_res;
+      p.pos_of[p.bs + 1] = c_ur;   // spans of the resident segment, per KV head
+      p.pos_of[p.bs + 2] = c_ua;   // of the arriving segment
     }
   }
   __syncthreads();
@@ -1084,45 +1130,49 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
     const Ranges& R = seg_b ? rb : ra;
     const int64_t off = seg_b ? ta : 0;
     const int64_t b = uniform64(off + R.begin(rid)), e = uniform64(off + R.end(rid));
+    const int64_t rid_k = seg_b ? p.num_waves + rid : rid;
     if (b < e)
       process_range<D, MT, NB, FUSE>(p, block_table, stage_table, seq_lens, q_indptr, s_pre,
-                                     s_order, total_q, seg_b ? p.num_waves + rid : rid, b, e,
-                                     lane, ob, !copy_mode);
+                                     s_order, total_q, rid_k, b, e, lane, ob, !copy_mode);
+    else
+      write_no_cut(p, rid_k, lane);
   }
   out_flush<D, MT>(p, ob, lane);
 }
 
 // Merge the partials of every item that a range boundary cut, in range order
-// (deterministic, no atomics).  One workgroup per (KV head, request); the
-// ranges holding the item's spans and their partial slots are found once per
-// workgroup.
+// (deterministic, no atomics).  One workgroup per range (of each segment):
+// it finishes the item the range cuts at its end, if that item began in the
+// range, from the range's record; the ranges holding the item's other parts
+// and their partial slots are found once per workgroup.
 template <int D, int MT, bool FUSE>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   constexpr int NB = span_blocks(D, MT, FUSE);
   __shared__ int64_t s_slot[256];   // partial slots of the item, in range order
   __shared__ int s_nslot;
-  const int g = blockIdx.x;
-  const int r = blockIdx.y;
-  const int hkv = p.num_kv_heads;
+  const int x = blockIdx.x;
   const int tid = threadIdx.x;
-  // the segment holding request r's position, and its ranges
-  const int n_res = (int)p.pos_of[p.bs];
-  const int pos = (int)p.pos_of[r];
-  const int64_t ta = (int64_t)hkv * p.prefix[n_res];
-  const bool seg_b = pos >= n_res;
+  const bool seg_b = x >= p.num_waves;
+  const int64_t q = seg_b ? x - p.num_waves : x;
+  const int hkv = p.num_kv_heads;
+  // all independent loads: the row count, the batch's spans, the record
+  const int total_q = p.q_indptr[p.bs];
+  const int64_t ta = (int64_t)hkv * p.pos_of[p.bs + 1];
+  const int64_t tb = (int64_t)hkv * p.pos_of[p.bs + 2];
+  const CutRec rec = p.cut_rec[x];
+  if (total_q <= 0) return;   // the main kernel attended nothing and wrote no record
+  const int64_t W = waves_for<NB, FUSE>(ta + tb, p.num_waves);
+  if (q >= W) return;         // no wave took this range: its record is stale
+  if (rec.n < 0 || rec.nq <= 0) return;
   const int64_t off = seg_b ? ta : 0;
   const int64_t qoff = seg_b ? p.num_waves : 0;
-  const int64_t W = waves_for<NB, FUSE>((int64_t)hkv * p.prefix[p.bs], p.num_waves);
-  const Ranges R(seg_b ? (int64_t)hkv * p.prefix[p.bs] - ta : ta, W, p.w_even,
-                 seg_b ? p.w_odd_b : p.w_odd);
-  const int L = clamp_len(p, p.seq_lens, r);
-  const int n = spans_of<NB>(L);
-  int qo, nq;
-  q_rows(p.q_indptr, r, max(0, p.q_indptr[p.bs]), p.max_q, qo, nq);
-  const int64_t base = (int64_t)p.prefix[pos] * hkv + (int64_t)g * n;
-  const int64_t ra = uniform64(R.of(base - off));           // first span's range
-  const int64_t rb = uniform64(R.of(base - off + n - 1));   // last span's range
-  if (ra == rb || nq == 0) return;
+  const Ranges R(seg_b ? tb : ta, W, p.w_even, seg_b ? p.w_odd_b : p.w_odd);
+  const int n = rec.n, g = rec.g, qo = rec.qo;
+  const int nq = min(rec.nq, max(0, total_q - qo));
+  const int64_t base = rec.base;
+  const int64_t ra = q;                                      // the item began in this range
+  const int64_t rb = uniform64(R.of(base - off + n - 1));   // its last span's range
+  if (rb <= ra || nq == 0) return;
   const int rows = p.group * nq;
   constexpr int kVec = D / 4;
   const int nel = rows * kVec;   // float4 elements of the item's rows
@@ -1231,7 +1281,7 @@ struct Plan {
   int mt;            // 16-row tiles
   int num_waves;     // W: resident waves of the launch
   size_t lds_bytes;  // dynamic LDS of the span prefix and work order
-  size_t prefix_bytes, part_o_bytes, part_ml_bytes, ws_bytes;
+  size_t prefix_bytes, part_o_bytes, part_ml_bytes, cut_rec_bytes, ws_bytes;
 };
 
 // Launch facts of one kernel instantiation on one device, queried once per
@@ -1239,8 +1289,10 @@ struct Plan {
 // keeps resident (CUs x workgroups per CU x 4), the LDS a workgroup may use
 // and the kernel's static LDS.
 struct KernelInfo {
-  int waves;
-  int lds_max;
+  int cus;
+  int blocks;         // workgroups per CU the registers allow (capped by waves_per_simd)
+  int lds_block;      // LDS one workgroup may address
+  int lds_cu;         // LDS of one CU
   size_t static_lds;
   bool ok;
 };
@@ -1257,21 +1309,28 @@ KernelInfo kernel_info(int d, int mt, bool fuse) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
     (void)hipGetLastError();
-    return KernelInfo{0, 0, 0, false};
+    return KernelInfo{0, 0, 0, 0, 0, false};
   }
   const int f = fuse ? 1 : 0, h = d == 128 ? 1 : 0, m = std::min(std::max(mt, 1), 4) - 1;
   std::lock_guard<std::mutex> lock(g_info_mu);
   if (g_info_set[dev][f][h][m]) return g_info[dev][f][h][m];
-  KernelInfo ki{0, 0, 0, false};
-  int cus = 0, blocks = 0;
+  KernelInfo ki{0, 0, 0, 0, 0, false};
+  int cus = 0, blocks = 0, lds_block = 0, lds_cu = 0;
   hipFuncAttributes fa;
   const void* k = fuse ? kernel_for<true>(d, mt) : kernel_for<false>(d, mt);
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, 256, 0) == hipSuccess &&
-      hipDeviceGetAttribute(&ki.lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
+      hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
           hipSuccess &&
-      hipFuncGetAttributes(&fa, k) == hipSuccess && cus > 0 && blocks > 0) {
-    ki.waves = cus * blocks * 4;
+      hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) ==
+          hipSuccess &&
+      hipFuncGetAttributes(&fa, k) == hipSuccess && cus > 0 && blocks > 0 && lds_cu > 0) {
+    // as many workgroups per CU as the registers allow, up to the waves per
+    // SIMD the kernel is compiled for
+    ki.cus = cus;
+    ki.blocks = std::min(blocks, waves_per_simd(d, mt, fuse));
+    ki.lds_block = lds_block;
+    ki.lds_cu = lds_cu;
     ki.static_lds = fa.sharedSizeBytes;
     ki.ok = true;
     g_info[dev][f][h][m] = ki;
@@ -1282,14 +1341,33 @@ KernelInfo kernel_info(int d, int mt, bool fuse) {
   return ki;
 }
 
+// Workgroups per CU for a launch whose span prefix and work order take
+// pre_bytes of LDS: the kernel's register limit, unless that leaves a
+// workgroup (with its share of the CU's LDS, so that all of them are resident
+// at once, as the static split assumes) too little room for four output
+// buffers of one record each; then fewer.
+int blocks_for(const KernelInfo& ki, int d, size_t pre_bytes) {
+  const size_t min_cap = d == 64 ? out_record_bytes<64>(kOutP, 16) : out_record_bytes<128>(kOutP, 16);
+  for (int b = ki.blocks; b > 1; --b)
+    if ((size_t)std::min(ki.lds_block, ki.lds_cu / b) >= ki.static_lds + pre_bytes + 4 * min_cap)
+      return b;
+  return 1;
+}
+
+// LDS one workgroup of the launch may use.
+int lds_budget(const KernelInfo& ki, int d, size_t pre_bytes) {
+  return std::min(ki.lds_block, ki.lds_cu / blocks_for(ki, d, pre_bytes));
+}
+
 // Waves a launch uses: the override when set, else the device's resident
-// waves (256 CUs x 2 workgroups when the device cannot be queried, which
-// only sizes a workspace query; a launch then fails on the LDS query).
-int resident_waves(int d, int mt, bool fuse) {
+// waves for this launch (256 CUs x 2 workgroups when the device cannot be
+// queried, which only sizes a workspace query; a launch then fails on the
+// LDS query).
+int resident_waves(int d, int mt, bool fuse, size_t pre_bytes) {
   const int w = g_waves_override.load(std::memory_order_relaxed);
   if (w > 0) return w;
   const KernelInfo ki = kernel_info(d, mt, fuse);
-  return ki.ok ? ki.waves : 256 * 2 * 4;
+  return ki.ok ? ki.cus * blocks_for(ki, d, pre_bytes) * 4 : 256 * 2 * 4;
 }
 
 bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool fuse,
@@ -1300,14 +1378,15 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool 
   const int rows = (hq / hkv) * max_q;
   if (rows > kMaxRows) return false;
   pl->mt = (rows + 15) / 16;
-  pl->num_waves = resident_waves(d, pl->mt, fuse);
+  pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t) + ((size_t)bs * sizeof(uint16_t) + 3) / 4 * 4;
+  pl->num_waves = resident_waves(d, pl->mt, fuse, (pl->lds_bytes + 15) / 16 * 16);
   // a head and a tail slot per range, W ranges in each of the two segments
   const size_t slots = 4 * (size_t)pl->num_waves * pl->mt * 16;
-  pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t) + ((size_t)bs * sizeof(uint16_t) + 3) / 4 * 4;
-  pl->prefix_bytes = (2 * ((size_t)bs + 1) * sizeof(uint32_t) + 255) / 256 * 256;
+  pl->prefix_bytes = ((2 * ((size_t)bs + 1) + 2) * sizeof(uint32_t) + 255) / 256 * 256;
   pl->part_o_bytes = slots * d * sizeof(float);
   pl->part_ml_bytes = slots * sizeof(float2);
-  pl->ws_bytes = pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes;
+  pl->cut_rec_bytes = 2 * (size_t)pl->num_waves * sizeof(CutRec);
+  pl->ws_bytes = pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes + pl->cut_rec_bytes;
   return true;
 }
 
@@ -1316,8 +1395,9 @@ void launch(const Params& p, int bs, size_t lds_bytes, hipStream_t stream) {
   hipLaunchKernelGGL((verify_attention_kernel<D, MT, FUSE>), dim3(p.num_waves / 4), dim3(256),
                      lds_bytes, stream, p, p.block_table, p.stage_table, p.seq_lens,
                      p.q_indptr);
-  hipLaunchKernelGGL((combine_kernel<D, MT, FUSE>), dim3(p.num_kv_heads, bs),
+  hipLaunchKernelGGL((combine_kernel<D, MT, FUSE>), dim3((FUSE ? 2 : 1) * p.num_waves),
                      dim3(256), 0, stream, p);
+  (void)bs;
 }
 
 template <int D, bool FUSE>
@@ -1374,8 +1454,8 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   // wave taking the rest of what a workgroup may have (at least one record)
   const KernelInfo ki = kernel_info(head_dim, pl.mt, fuse);
   if (!ki.ok) return fail(NSD_ERR_HIP, "%s: the device's LDS size could not be queried", fn);
-  const int lds_max = ki.lds_max;
   const size_t pre_bytes = (pl.lds_bytes + 15) / 16 * 16;
+  const int lds_max = lds_budget(ki, head_dim, pre_bytes);
   const size_t fixed = ki.static_lds + pre_bytes;
   const size_t per_wave = (size_t)lds_max > fixed ? ((size_t)lds_max - fixed) / 4 / 16 * 16 : 0;
   const size_t min_cap = head_dim == 64 ? out_record_bytes<64>(kOutP, 16)
@@ -1402,6 +1482,7 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   p.pos_of = p.prefix + bs + 1;
   p.part_o = (float*)(ws + pl.prefix_bytes);
   p.part_ml = (float2*)(ws + pl.prefix_bytes + pl.part_o_bytes);
+  p.cut_rec = (CutRec*)(ws + pl.prefix_bytes + pl.part_o_bytes + pl.part_ml_bytes);
   p.num_blocks = (int32_t)num_blocks;
   p.stage_blocks = fuse ? (int32_t)stage_blocks : 0;
   p.bs = bs;
