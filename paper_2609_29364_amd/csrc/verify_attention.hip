@@ -43,7 +43,9 @@
 //   resident and the arriving requests' spans separately and every wave takes
 //   one range of each, resident first, so that all waves write the staged
 //   tiles in the same phase of the launch (writes gathered in time cost HBM
-//   less than writes spread through the read stream).  The split is static:
+//   less than writes spread through the read stream).  The resident segment
+//   only reads, so it streams the separate attention's deeper spans; the
+//   arriving segment's spans are sized for the tile that also stores.  The split is static:
 //   the workspace needs no initialisation and no wave waits on another.
 //   Items cut by a range boundary leave partials that a small second kernel
 //   merges in range order (deterministic, no atomics in the arithmetic); all
@@ -79,14 +81,17 @@ constexpr int kMaxRows = 64;      // (Hq/Hkv) * max_q_per_seq limit
 constexpr int kMaxBatch = 8192;   // the span prefix of the batch lives in LDS
 constexpr int kSpare = -1;        // span index of loads that are never used
 
-// Blocks per main-loop step for a (head_dim, row tiles, fused) instantiation:
-// four where the registers of two extra K/V tiles fit beside the
-// accumulators.  The fused tile also holds its store path: with four blocks
+// Blocks per main-loop step for a (head_dim, row tiles) tile, reading only
+// (store = false: the separate attention and the fused pass's resident
+// segment) or also writing the tiles back (the fused pass's arriving
+// segment): four where the registers of two extra K/V tiles fit beside the
+// accumulators.  The writing tile also holds its store path: with four blocks
 // and more than one 16-row tile at head_dim 128 it ran out of registers and
 // reloaded a spilled lane offset before every span's loads (waiting for all
-// of them), so it takes two.
-__host__ __device__ constexpr int span_blocks(int d, int mt, bool fuse) {
-  return (fuse && d * mt > 128) ? 2 : (d * mt <= 256 ? 4 : 2);
+// of them), so it takes two.  The two segments of the fused pass are split
+// into ranges separately, so each takes its own span size.
+__host__ __device__ constexpr int span_blocks(int d, int mt, bool store) {
+  return (store && d * mt > 128) ? 2 : (d * mt <= 256 ? 4 : 2);
 }
 
 // Waves per SIMD an instantiation is compiled for, and the most its launch
@@ -258,7 +263,7 @@ struct Item {
   bool arriving;     // fused variant: K/V come from the staging pool
 };
 
-template <int NB, bool FUSE>
+template <int NB, bool ARR>
 __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
                                  const int32_t* __restrict__ stage_table, int pos, int r,
@@ -270,7 +275,7 @@ __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ se
   it.pr = pr;
   it.L = clamp_len(p, seq_lens, r);
   it.n = spans_of<NB>(it.L);
-  it.arriving = FUSE && is_arriving(p, stage_table, r);
+  it.arriving = ARR;
   it.base = (int64_t)p.num_kv_heads * pr + (int64_t)g * it.n;
   spans_in(it.base, it.n, s, s1, it.j0, it.j1);
   q_rows(q_indptr, r, total_q, p.max_q, it.qo, it.nq);
@@ -280,17 +285,17 @@ __device__ inline Item make_item(const Params& p, const int32_t* __restrict__ se
 }
 
 // The item after `it` in (position, KV head) order; `it` is not the last
-// item of the order.
-template <int NB, bool FUSE>
+// item of the order.  ORD: positions map to requests through the work order.
+template <int NB, bool ORD, bool ARR>
 __device__ inline Item next_item(const Params& p, const int32_t* __restrict__ seq_lens,
                                  const int32_t* __restrict__ q_indptr,
                                  const int32_t* __restrict__ stage_table, const uint16_t* order,
                                  const Item& it, int64_t s, int64_t s1, int total_q) {
   const bool nr = it.g == p.num_kv_heads - 1;
   const int pos = nr ? it.pos + 1 : it.pos;
-  return make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos,
-                             nr ? uniform(request_at<FUSE>(order, pos)) : it.r, nr ? 0 : it.g + 1,
-                             nr ? it.pr + it.n : it.pr, s, s1, total_q);
+  return make_item<NB, ARR>(p, seq_lens, q_indptr, stage_table, pos,
+                            nr ? uniform(request_at<ORD>(order, pos)) : it.r, nr ? 0 : it.g + 1,
+                            nr ? it.pr + it.n : it.pr, s, s1, total_q);
 }
 
 // Raw block-table entries of one span (scalar loads, checked later).
@@ -314,19 +319,19 @@ struct SpanRef {
 // are fetched with scalar loads, which keep the vector-memory counter free
 // for the K/V stream; the indexes are clamped into the row, so the loads are
 // unconditional.
-template <int NB, bool FUSE>
+template <int NB, bool ARR>
 __device__ inline SpanIds<NB> load_ids(const Params& p, const int32_t* __restrict__ block_table,
                                        const int32_t* __restrict__ stage_table, const Item& it,
                                        int j) {
   SpanIds<NB> ids;
   const int64_t row = (int64_t)it.r * p.max_blocks_per_seq;
   const int last = p.max_blocks_per_seq - 1;
-  const int32_t* __restrict__ src = (FUSE && it.arriving) ? stage_table : block_table;
+  const int32_t* __restrict__ src = ARR ? stage_table : block_table;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     const int e = min(j * NB + b, last);
     ids.src[b] = src[row + e];
-    ids.dst[b] = FUSE ? block_table[row + e] : -1;
+    ids.dst[b] = ARR ? block_table[row + e] : -1;
   }
   return ids;
 }
@@ -334,7 +339,7 @@ __device__ inline SpanIds<NB> load_ids(const Params& p, const int32_t* __restric
 // Span j of item it from its table entries.  Blocks past the context reuse
 // block 0's tile (their tokens are masked) and are not written by the fused
 // variant, nor are arriving blocks with an invalid staging or destination id.
-template <int NB, bool FUSE>
+template <int NB, bool ARR>
 __device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
                                        const SpanIds<NB>& ids) {
   SpanRef<NB> s;
@@ -343,7 +348,7 @@ __device__ inline SpanRef<NB> make_ref(const Params& p, const Item& it, int j,
   s.t = spare ? 0 : j * NB * kBlock;
   s.bad = 0;
   const int nb = max(1, min(NB, (it.L - s.t + kBlock - 1) / kBlock));
-  const bool arr = FUSE && it.arriving;
+  const bool arr = ARR;
   s.k_src = arr ? p.k_stage : p.k_cache;
   s.v_src = arr ? p.v_stage : p.v_cache;
   const int32_t src_blocks = arr ? p.stage_blocks : p.num_blocks;
@@ -579,7 +584,7 @@ __device__ inline void span_pv(const VOps<D, NB>& v, const SpanRef<NB>& s, int L
 // refilled with nit's Q before its first K/V loads are issued: the loads
 // complete in order, so waiting for that K also covers Q, and the switch to
 // the next item waits for nothing.
-template <int D, int MT, int NB, bool FUSE, bool STORE, bool NEXTQ>
+template <int D, int MT, int NB, bool ARR, bool STORE, bool NEXTQ>
 __device__ inline void span_step(KOps<D, NB>& kr, VOps<D, NB>& vr, SpanRef<NB>& cur,
                                  const Item& nit, int nj, const SpanIds<NB>& nids,
                                  QOps<MT, D>& q, const Params& p, Acc<D, MT>& a, int win, int L,
@@ -591,7 +596,7 @@ __device__ inline void span_step(KOps<D, NB>& kr, VOps<D, NB>& vr, SpanRef<NB>& 
   // entries) behind the score products
   __builtin_amdgcn_sched_barrier(0);
   if constexpr (NEXTQ) load_q<D, MT>(q, p, nit, total_q, lane);
-  const SpanRef<NB> nr = make_ref<NB, FUSE>(p, nit, nj, nids);
+  const SpanRef<NB> nr = make_ref<NB, ARR>(p, nit, nj, nids);
   load_k<D, NB>(kr, nr, lane);
   bf16x8 pop[NB / 2][MT];
   span_softmax<D, MT, NB>(st, cur, a, win, p.scale_log2, lane, pop);
@@ -769,8 +774,9 @@ struct Ranges {
   }
 };
 
-// Waves a launch of W waves uses for a batch of T spans of NB blocks (B = T
-// NB blocks), a multiple of 4, at least kMinWaves, at most W.  A small batch
+// Waves a launch of W waves uses for a batch of B blocks (per KV head, over
+// the segments' spans: ta spans of the reading tile's blocks, tb of the
+// writing tile's), a multiple of 4, at least kMinWaves, at most W.  A small batch
 // spread over every resident wave cuts each item into one-span parts whose
 // merge costs more than the streaming (a one-request round ran in 65 us on
 // 1024 waves and 29 us on 64); too few waves leave HBM idle.  Measured on
@@ -778,13 +784,18 @@ struct Ranges {
 // wave per 20 blocks; the fused pass at B / (15 + B / 1000) waves (about 15
 // blocks per wave at 1k blocks, 30 at 10-20k, 80 at 60k), and with every
 // resident wave once that passes 7/8 of them.  Every kernel derives the
-// same count from T.
+// same count from the segments' spans.
 constexpr int kMinWaves = 64;
 constexpr int kMinCopyWaves = 64;   // surplus waves that take over the fused pass's pool writes
 
-template <int NB, bool FUSE>
-__device__ inline int64_t waves_for(int64_t T, int64_t W) {
-  const int64_t B = T * NB;
+template <int D, int MT>
+__device__ inline int64_t segment_blocks(int64_t ta, int64_t tb) {
+  return ta * span_blocks(D, MT, false) + tb * span_blocks(D, MT, true);
+}
+
+template <int D, int MT, bool FUSE>
+__device__ inline int64_t waves_for(int64_t ta, int64_t tb, int64_t W) {
+  const int64_t B = segment_blocks<D, MT>(ta, tb);
   int64_t want = FUSE ? B * 1000 / (15000 + B) : (B + 19) / 20;
   if (FUSE && 8 * want > 7 * W) want = W;
   return min(W, max((int64_t)kMinWaves, (want + 3) / 4 * 4));
@@ -808,12 +819,12 @@ __device__ inline int first_or_spare(const Item& it, const Item& next) {
 
 // Table entries of the span after span j of `it`: span j+1, or next's first
 // span when j is the item's last (when next is it, unused).
-template <int NB, bool FUSE>
+template <int NB, bool ARR>
 __device__ inline SpanIds<NB> ids_after(const Params& p, const int32_t* __restrict__ block_table,
                                         const int32_t* __restrict__ stage_table, const Item& it,
                                         const Item& next, int j) {
-  return j + 1 < it.j1 ? load_ids<NB, FUSE>(p, block_table, stage_table, it, j + 1)
-                       : load_ids<NB, FUSE>(p, block_table, stage_table, next, next.j0);
+  return j + 1 < it.j1 ? load_ids<NB, ARR>(p, block_table, stage_table, it, j + 1)
+                       : load_ids<NB, ARR>(p, block_table, stage_table, next, next.j0);
 }
 
 // Spans [j0, j1) of one item.  The loads of the item's first span were issued
@@ -823,23 +834,23 @@ __device__ inline SpanIds<NB> ids_after(const Params& p, const int32_t* __restri
 // read block 0's tile of the item's KV head, which every wave's spare loads
 // share, so they come from the L2 rather than HBM.
 // Table entries are fetched one step before the step that uses them.
-template <int D, int MT, int NB, bool FUSE, bool ARR>
+template <int D, int MT, int NB, bool ARR, bool STORE>
 __device__ inline void run_item(const Params& p, const int32_t* __restrict__ block_table,
                                 const int32_t* __restrict__ stage_table, const Item& it,
                                 const Item& next, KOps<D, NB>& kreg, VOps<D, NB>& vreg,
                                 SpanRef<NB>& cur, QOps<MT, D>& q, Acc<D, MT>& a, int total_q,
                                 int lane) {
-  SpanIds<NB> ids = ids_after<NB, FUSE>(p, block_table, stage_table, it, next, it.j0);
+  SpanIds<NB> ids = ids_after<NB, ARR>(p, block_table, stage_table, it, next, it.j0);
   for (int j = it.j0; j + 1 < it.j1; ++j) {
-    const SpanIds<NB> ids2 = ids_after<NB, FUSE>(p, block_table, stage_table, it, next, j + 1);
-    span_step<D, MT, NB, FUSE, ARR, false>(kreg, vreg, cur, it, j + 1, ids, q, p, a, it.win, it.L,
-                                           total_q, lane);
+    const SpanIds<NB> ids2 = ids_after<NB, ARR>(p, block_table, stage_table, it, next, j + 1);
+    span_step<D, MT, NB, ARR, STORE, false>(kreg, vreg, cur, it, j + 1, ids, q, p, a, it.win,
+                                            it.L, total_q, lane);
     ids = ids2;
   }
-  // the last span also brings in the next item's first K/V, and (without
-  // fusion) its Q; the fused tile has no registers to spare there (its Q
+  // the last span also brings in the next item's first K/V, and (reading
+  // only) its Q; the writing tile has no registers to spare there (its Q
   // loaded here spilled and cost 4 %), so it loads Q at the switch
-  span_step<D, MT, NB, FUSE, ARR, !FUSE>(kreg, vreg, cur, next, first_or_spare(it, next), ids, q,
+  span_step<D, MT, NB, ARR, STORE, !ARR>(kreg, vreg, cur, next, first_or_spare(it, next), ids, q,
                                          p, a, it.win, it.L, total_q, lane);
 }
 
@@ -864,8 +875,11 @@ __device__ __attribute__((always_inline)) inline void write_no_cut(const Params&
 }
 
 // One range [s, s1) of global spans, range id rid: online softmax over every
-// (request, KV head) item the range touches.
-template <int D, int MT, int NB, bool FUSE>
+// (request, KV head) item the range touches.  ORD: positions map to requests
+// through the fused pass's work order; ARR: the range lies in the arriving
+// segment (tiles read from the staging pool and, with `store`, written to the
+// worker pool).
+template <int D, int MT, int NB, bool ORD, bool ARR>
 __device__ void process_range(const Params& p, const int32_t* __restrict__ block_table,
                               const int32_t* __restrict__ stage_table,
                               const int32_t* __restrict__ seq_lens,
@@ -874,36 +888,37 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
                               int64_t s1, int lane, OutBuf& ob, bool store) {
   const int hkv = p.num_kv_heads;
   const int pos0 = uniform(find_position(pre, p.bs, hkv, s));
-  const int r0 = uniform(request_at<FUSE>(order, pos0));
+  const int r0 = uniform(request_at<ORD>(order, pos0));
   const int64_t pr0 = uniform64(pre[pos0]);
   // the item holding span position s
   const int n0 = spans_of<NB>(clamp_len(p, seq_lens, r0));
   const int g0 = (int)min((int64_t)hkv - 1, (s - (int64_t)hkv * pr0) / n0);
-  Item it = make_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, pos0, r0, g0, pr0, s, s1,
-                                total_q);
+  Item it = make_item<NB, ARR>(p, seq_lens, q_indptr, stage_table, pos0, r0, g0, pr0, s, s1,
+                               total_q);
   if (it.j0 >= it.j1) {
     if (it.pos == p.bs - 1 && it.g == hkv - 1) return write_no_cut(p, rid, lane);
-    it = next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, it, s, s1, total_q);
+    it = next_item<NB, ORD, ARR>(p, seq_lens, q_indptr, stage_table, order, it, s, s1, total_q);
     if (it.j0 >= it.j1) return write_no_cut(p, rid, lane);   // no span lies here
   }
   // next item with a span in the range (or `it` itself when none)
   auto following = [&](const Item& cur) {
     const bool last = cur.pos == p.bs - 1 && cur.g == hkv - 1;
     if (last || cur.base + (int64_t)cur.n >= s1) return cur;
-    return next_item<NB, FUSE>(p, seq_lens, q_indptr, stage_table, order, cur, s, s1, total_q);
+    return next_item<NB, ORD, ARR>(p, seq_lens, q_indptr, stage_table, order, cur, s, s1,
+                                   total_q);
   };
   Item next = following(it);
   bool more = next.base != it.base;
 
-  // the first item's Q; without fusion each later item's Q comes with its
+  // the first item's Q; reading only, each later item's Q comes with its
   // first K/V loads, during the previous item's last span (one set of Q
   // registers: a second copy for a prefetch one item ahead spilled in the
-  // fused tile, and moving it between register files made the wave wait for
-  // all its loads at every item switch)
+  // writing tile, and moving it between register files made the wave wait
+  // for all its loads at every item switch)
   QOps<MT, D> qc;
   load_q<D, MT>(qc, p, it, total_q, lane);
   SpanRef<NB> cur =
-      make_ref<NB, FUSE>(p, it, it.j0, load_ids<NB, FUSE>(p, block_table, stage_table, it, it.j0));
+      make_ref<NB, ARR>(p, it, it.j0, load_ids<NB, ARR>(p, block_table, stage_table, it, it.j0));
   KOps<D, NB> kreg;
   VOps<D, NB> vreg;
   load_k<D, NB>(kreg, cur, lane);
@@ -911,12 +926,12 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
   while (true) {
     Acc<D, MT> a;
     init_acc<D, MT>(a, p, it, lane);
-    if (FUSE && it.arriving && store)
-      run_item<D, MT, NB, FUSE, true>(p, block_table, stage_table, it, next, kreg, vreg, cur,
-                                      qc, a, total_q, lane);
+    if (ARR && store)
+      run_item<D, MT, NB, ARR, ARR>(p, block_table, stage_table, it, next, kreg, vreg, cur, qc, a,
+                                    total_q, lane);
     else
-      run_item<D, MT, NB, FUSE, false>(p, block_table, stage_table, it, next, kreg, vreg, cur,
-                                       qc, a, total_q, lane);
+      run_item<D, MT, NB, ARR, false>(p, block_table, stage_table, it, next, kreg, vreg, cur, qc,
+                                      a, total_q, lane);
     finish_item<D, MT>(p, a, it, rid, lane, ob);
     if (!more) {
       // the range's last item, if it began here and continues past the range
@@ -924,9 +939,9 @@ __device__ void process_range(const Params& p, const int32_t* __restrict__ block
       write_cut_rec(p, rid, lane, cut, it.base, it.n, it.r, it.g, it.qo, it.nq);
       break;
     }
-    // switch to the next item (its first span, and Q without fusion, are
+    // switch to the next item (its first span, and Q when reading only, are
     // already requested)
-    if constexpr (FUSE) load_q<D, MT>(qc, p, next, total_q, lane);
+    if constexpr (ARR) load_q<D, MT>(qc, p, next, total_q, lane);
     it = next;
     next = following(it);
     more = next.base != it.base;
@@ -1011,7 +1026,8 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
                              const int32_t* __restrict__ stage_table,
                              const int32_t* __restrict__ seq_lens,
                              const int32_t* __restrict__ q_indptr) {
-  constexpr int NB = span_blocks(D, MT, FUSE);
+  constexpr int NBA = span_blocks(D, MT, false);   // resident (or only) segment
+  constexpr int NBB = span_blocks(D, MT, true);    // arriving segment
   extern __shared__ uint32_t s_pre[];   // [bs + 1] span prefix by position, then uint16 order[bs]
   uint16_t* s_order = (uint16_t*)(s_pre + p.bs + 1);
   __shared__ uint32_t s_wsum[3][4];
@@ -1029,7 +1045,7 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
     for (int r = tid; r < p.bs; r += 256)
       if (!is_arriving(p, stage_table, r)) {
         ++c;
-        u += spans_of<NB>(clamp_len(p, seq_lens, r));
+        u += spans_of<NBA>(clamp_len(p, seq_lens, r));
       }
     n_res = block_sum(c, s_red, lane, wave);
     u_res = block_sum(u, s_red, lane, wave);
@@ -1042,7 +1058,8 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
     const int r = base + tid;
     const bool in = r < p.bs;
     const bool arr = in && FUSE && is_arriving(p, stage_table, r);
-    const uint32_t n = in ? spans_of<NB>(clamp_len(p, seq_lens, r)) : 0;
+    const int L = in ? clamp_len(p, seq_lens, r) : 0;
+    const uint32_t n = in ? (arr ? spans_of<NBB>(L) : spans_of<NBA>(L)) : 0;
     uint32_t v[3] = {arr ? 1u : 0u, arr ? n : 0u, arr ? 0u : n};
     uint32_t incl[3] = {v[0], v[1], v[2]};
 #pragma unroll
@@ -1097,11 +1114,11 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
     // still move to the worker pool (the preparation does not depend on the
     // queries), copied by every wave
     if (FUSE && tb > 0)
-      copy_staged<D, NB>(p, block_table, stage_table, seq_lens, s_pre, s_order, (int)n_res, rid,
-                         p.num_waves, lane);
+      copy_staged<D, NBB>(p, block_table, stage_table, seq_lens, s_pre, s_order, (int)n_res, rid,
+                          p.num_waves, lane);
     return;
   }
-  const int64_t W = waves_for<NB, FUSE>(ta + tb, p.num_waves);
+  const int64_t W = waves_for<D, MT, FUSE>(ta, tb, p.num_waves);
   // a batch too small for every resident wave: the surplus waves write the
   // staged blocks to the worker pool, so the attention waves stream without
   // stores, when there are enough of them and the batch is small enough for
@@ -1109,12 +1126,13 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
   // copy wave at most 0.4 of the attention's per wave; measured: 4 requests
   // 6 % faster, 8 requests 3 %, 16 requests 21 % slower without that bound)
   const int64_t ncopy = p.num_waves - W;
-  const bool copy_mode =
-      FUSE && tb > 0 && ncopy >= kMinCopyWaves && 5 * tb * W <= (ta + tb) * ncopy;
+  const int64_t tb_blocks = tb * NBB;
+  const bool copy_mode = FUSE && tb > 0 && ncopy >= kMinCopyWaves &&
+                         5 * tb_blocks * W <= segment_blocks<D, MT>(ta, tb) * ncopy;
   if (rid >= W) {
     if (copy_mode)
-      copy_staged<D, NB>(p, block_table, stage_table, seq_lens, s_pre, s_order, (int)n_res,
-                      rid - W, ncopy, lane);
+      copy_staged<D, NBB>(p, block_table, stage_table, seq_lens, s_pre, s_order, (int)n_res,
+                          rid - W, ncopy, lane);
     return;
   }
   const Ranges ra(ta, W, p.w_even, p.w_odd), rb(tb, W, p.w_even, p.w_odd_b);
@@ -1123,21 +1141,35 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
   ob.base = (char*)s_pre + p.out_off + wave * p.out_cap;
   ob.cap = p.out_cap;
   ob.used = 0;
-  // resident range first, then the arriving range (writes last)
-#pragma unroll 1
-  for (int k = 0; k < (FUSE ? 2 : 1); ++k) {
-    const bool seg_b = k == 1;
-    const Ranges& R = seg_b ? rb : ra;
-    const int64_t off = seg_b ? ta : 0;
-    const int64_t b = uniform64(off + R.begin(rid)), e = uniform64(off + R.end(rid));
-    const int64_t rid_k = seg_b ? p.num_waves + rid : rid;
+  // resident range first (reading only, the reading tile's spans), then the
+  // arriving range (writes last, the writing tile's spans)
+  {
+    const int64_t b = uniform64(ra.begin(rid)), e = uniform64(ra.end(rid));
     if (b < e)
-      process_range<D, MT, NB, FUSE>(p, block_table, stage_table, seq_lens, q_indptr, s_pre,
-                                     s_order, total_q, rid_k, b, e, lane, ob, !copy_mode);
+      process_range<D, MT, NBA, FUSE, false>(p, block_table, stage_table, seq_lens, q_indptr,
+                                             s_pre, s_order, total_q, rid, b, e, lane, ob, false);
     else
-      write_no_cut(p, rid_k, lane);
+      write_no_cut(p, rid, lane);
+  }
+  if constexpr (FUSE) {
+    const int64_t b = uniform64(ta + rb.begin(rid)), e = uniform64(ta + rb.end(rid));
+    const int64_t rid_b = p.num_waves + rid;
+    if (b < e)
+      process_range<D, MT, NBB, true, true>(p, block_table, stage_table, seq_lens, q_indptr,
+                                            s_pre, s_order, total_q, rid_b, b, e, lane, ob,
+                                            !copy_mode);
+    else
+      write_no_cut(p, rid_b, lane);
   }
   out_flush<D, MT>(p, ob, lane);
+}
+
+// Threads per row of the merge kernel's 256: a power of two dividing the
+// row's float4 count, with every row of a 16-row-tile item covered.
+__host__ __device__ constexpr int merge_threads_per_row(int vec, int rows) {
+  int t = 1;
+  while (t * 2 <= 256 / rows && t * 2 <= vec) t *= 2;
+  return t;
 }
 
 // Merge the partials of every item that a range boundary cut, in range order
@@ -1147,7 +1179,6 @@ void verify_attention_kernel(Params p, const int32_t* __restrict__ block_table,
 // and their partial slots are found once per workgroup.
 template <int D, int MT, bool FUSE>
 __global__ __launch_bounds__(256) void combine_kernel(Params p) {
-  constexpr int NB = span_blocks(D, MT, FUSE);
   __shared__ int64_t s_slot[256];   // partial slots of the item, in range order
   __shared__ int s_nslot;
   const int x = blockIdx.x;
@@ -1161,7 +1192,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const int64_t tb = (int64_t)hkv * p.pos_of[p.bs + 2];
   const CutRec rec = p.cut_rec[x];
   if (total_q <= 0) return;   // the main kernel attended nothing and wrote no record
-  const int64_t W = waves_for<NB, FUSE>(ta + tb, p.num_waves);
+  const int64_t W = waves_for<D, MT, FUSE>(ta, tb, p.num_waves);
   if (q >= W) return;         // no wave took this range: its record is stale
   if (rec.n < 0 || rec.nq <= 0) return;
   const int64_t off = seg_b ? ta : 0;
@@ -1174,19 +1205,21 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
   const int64_t rb = uniform64(R.of(base - off + n - 1));   // its last span's range
   if (rb <= ra || nq == 0) return;
   const int rows = p.group * nq;
+  // thread layout: kTPR threads per row, each holding kPer float4 elements of
+  // it (lane-contiguous per element index), so a thread reads one (max, sum)
+  // per part; few registers, so every range's workgroup is resident at once
   constexpr int kVec = D / 4;
-  const int nel = rows * kVec;   // float4 elements of the item's rows
-  // running merge over the ranges, 256 at a time (an item rarely spans more
-  // than a few)
-  constexpr int kPer = (MT * 16 * kVec + 255) / 256;   // elements per thread
-  float mrun[kPer], drun[kPer];
+  constexpr int kTPR = merge_threads_per_row(kVec, MT * 16);
+  constexpr int kPer = kVec / kTPR;
+  const int m = tid / kTPR;                 // this thread's row (idle when >= rows)
+  const int c = tid % kTPR;
+  const int mld = min(m, rows - 1);         // loads clamped into the item's rows
+  float mrun = -INFINITY, drun = 0.f;
   f32x4 orun[kPer];
 #pragma unroll
-  for (int i = 0; i < kPer; ++i) {
-    mrun[i] = -INFINITY;
-    drun[i] = 0.f;
-    orun[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int i = 0; i < kPer; ++i) orun[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // running merge over the ranges, 256 at a time (an item rarely spans more
+  // than a few)
   for (int64_t q0 = ra; q0 <= rb; q0 += 256) {
     const int64_t q = q0 + tid;
     if (q <= rb) {
@@ -1204,53 +1237,45 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
     }
     __syncthreads();
     const int cnt = s_nslot;
-    // two parts at a time (a cut item has two in most cases): every load of
-    // the thread's elements is issued before the first merge (addresses
-    // clamped into the item's rows)
+    // two parts at a time (a cut item has two in most cases): every load is
+    // issued before the first merge
     for (int k0 = 0; k0 < cnt; k0 += 2) {
-      float2 ml[kPer][2];
-      f32x4 o[kPer][2];
+      float2 ml[2];
+      f32x4 o[2][kPer];
 #pragma unroll
-      for (int i = 0; i < kPer; ++i) {
-        const int idx = min(tid + i * 256, nel - 1);
-        const int m = idx / kVec;
-        const int d = (idx % kVec) * 4;
+      for (int u = 0; u < 2; ++u) {
+        const int64_t slot = s_slot[min(k0 + u, cnt - 1)];
+        const int64_t row = slot * (MT * 16) + mld;
+        ml[u] = p.part_ml[row];
+        const f32x4* src = (const f32x4*)(p.part_o + row * D) + c;
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int64_t slot = s_slot[min(k0 + u, cnt - 1)];
-          ml[i][u] = p.part_ml[slot * (MT * 16) + m];
-          o[i][u] = *(const f32x4*)(p.part_o + (slot * (MT * 16) + m) * D + d);
-        }
+        for (int i = 0; i < kPer; ++i) o[u][i] = src[i * kTPR];
       }
 #pragma unroll
-      for (int i = 0; i < kPer; ++i) {
+      for (int u = 0; u < 2; ++u) {
+        if (k0 + u >= cnt || ml[u].x == -INFINITY) continue;   // no visible token there
+        const float mx = fmaxf(mrun, ml[u].x);
+        const float a = mrun == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun - mx);
+        const float b = __builtin_amdgcn_exp2f(ml[u].x - mx);
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          if (k0 + u >= cnt || ml[i][u].x == -INFINITY) continue;   // no visible token there
-          const float mx = fmaxf(mrun[i], ml[i][u].x);
-          const float a = mrun[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun[i] - mx);
-          const float b = __builtin_amdgcn_exp2f(ml[i][u].x - mx);
-          orun[i] = a * orun[i] + b * o[i][u];
-          drun[i] = a * drun[i] + b * ml[i][u].y;
-          mrun[i] = mx;
-        }
+        for (int i = 0; i < kPer; ++i) orun[i] = a * orun[i] + b * o[u][i];
+        drun = a * drun + b * ml[u].y;
+        mrun = mx;
       }
     }
     __syncthreads();
   }
+  if (m >= rows) return;
+  const float inv = drun > 0.f ? 1.f / drun : 0.f;
+  const int j = m / p.group;
+  const int h = g * p.group + m % p.group;
+  uint16_t* dst = p.out + ((int64_t)(qo + j) * p.num_q_heads + h) * D;
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
-    const int idx = tid + i * 256;
-    if (idx >= nel) continue;
-    const int m = idx / kVec;
-    const int d = (idx % kVec) * 4;
-    const float inv = drun[i] > 0.f ? 1.f / drun[i] : 0.f;
-    const int j = m / p.group;
-    const int h = g * p.group + m % p.group;
-    uint16_t* dst = p.out + ((int64_t)(qo + j) * p.num_q_heads + h) * D + d;
     const bf16x2 lo = {(__bf16)(orun[i][0] * inv), (__bf16)(orun[i][1] * inv)};
     const bf16x2 hi = {(__bf16)(orun[i][2] * inv), (__bf16)(orun[i][3] * inv)};
-    *(u32x2*)dst = u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+    *(u32x2*)(dst + (i * kTPR + c) * 4) =
+        u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
   }
 }
 
