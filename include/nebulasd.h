@@ -313,10 +313,15 @@ nsd_status nsd_writeback_pairs(const int32_t* block_table, int32_t max_blocks_pe
  * Row q_indptr[r] + j of k_new / v_new (bf16 [total_q][num_kv_heads][head_dim])
  * is window token j of request r, at position t = seq_lens[r] - n_q + j; it is
  * written to slot t % 16 of block block_table[r][t / 16] of k_pool / v_pool
- * (this layer's planes, layout above), every KV head.  Nothing else is
- * written.  Positions outside [0, 16 * max_blocks_per_seq) and block ids
- * outside [0, num_blocks) are skipped.  block_size == 16, head_dim in {64, 128}.
- * bs == 0 or total_q == 0 is a no-op.
+ * (this layer's planes, layout above), every KV head.  No other slot
+ * changes: the kernel writes whole 32-byte sectors (a V row's 16 slots, a K
+ * run pair), so the other slots of a sector the window touches are written
+ * back with their own contents, and no other operation may write those
+ * blocks while the call runs.  Positions outside [0, 16 * max_blocks_per_seq)
+ * and block ids outside [0, num_blocks) are skipped; two requests naming one
+ * block give unspecified contents in it.  k_pool and v_pool are 16-byte
+ * aligned (NSD_ERR_SHAPE otherwise).  block_size == 16, head_dim in
+ * {64, 128}.  bs == 0 or total_q == 0 is a no-op.
  */
 nsd_status nsd_kv_append(void* k_pool, void* v_pool, int64_t num_blocks, const void* k_new,
                          const void* v_new, const int32_t* block_table,

@@ -8,13 +8,45 @@
 // its n_r accepted proposals: L'_r = L_r - K_r + n_r (the resampled or bonus
 // token is the next round's anchor).
 //
-// kv_append: one workgroup per (KV head, request), one lane per dimension;
-// the lanes of a 16-byte K run write one contiguous run, V elements land at
-// their slot of each dimension's 16-slot row.  The volume is the window only
-// (verify_8b: 1280 rows x 8 heads x 128 dims x 2 planes x 2 bytes = 5 MB).
+// kv_append: one workgroup per (KV head, request).  Memory writes whole
+// 32-byte sectors cheaply and partial ones with a read-modify-write in the
+// memory system, which also delays the kernels that follow (a decode
+// attention launched right after an append made of 2-byte element stores
+// ran 6 % slower).  So the kernel writes whole sectors only: for every block
+// the window touches, thread d rewrites dimension d's 16-slot V row (32
+// bytes) and thread (run c, slot pair) the two 16-byte K runs of a slot
+// pair, taking the window's slots from the new rows and every other slot
+// from the sector's current contents.  Only this workgroup writes the
+// (block, KV head) tile, so the merge needs no ordering.  Volume: the
+// sectors the window touches, read and written (about 4.5 KiB each way per
+// (request, KV head) for a one-token window at head_dim 128, 13 MB each way
+// for a verify_8b layer's five-token windows).
 #include "nsd_internal.h"
 
 namespace {
+
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
+// 32 bytes as 16 bf16 (two 16-byte accesses)
+struct Sector {
+  uint16_t e[16];
+};
+
+__device__ inline Sector load_sector(const uint16_t* p) {
+  Sector s;
+  const u32x4 a = ((const u32x4*)p)[0], b = ((const u32x4*)p)[1];
+  __builtin_memcpy(&s.e[0], &a, 16);
+  __builtin_memcpy(&s.e[8], &b, 16);
+  return s;
+}
+
+__device__ inline void store_sector(uint16_t* p, const Sector& s) {
+  u32x4 a, b;
+  __builtin_memcpy(&a, &s.e[0], 16);
+  __builtin_memcpy(&b, &s.e[8], 16);
+  ((u32x4*)p)[0] = a;
+  ((u32x4*)p)[1] = b;
+}
 
 __global__ __launch_bounds__(128) void kv_append_kernel(
     uint16_t* __restrict__ k_pool, uint16_t* __restrict__ v_pool,
@@ -24,22 +56,52 @@ __global__ __launch_bounds__(128) void kv_append_kernel(
     int32_t num_kv_heads, int32_t head_dim, int32_t total_q) {
   const int g = blockIdx.x;
   const int r = blockIdx.y;
-  const int d = threadIdx.x;
-  if (d >= head_dim) return;
+  const int tid = threadIdx.x;
   const int a = q_indptr[r];
   const int nq = q_indptr[r + 1] - a;
   const int L = seq_lens[r];
-  for (int j = 0; j < nq; ++j) {
-    const int t = L - nq + j;
-    const int row = a + j;
-    if (t < 0 || t >= max_blocks_per_seq * 16 || row < 0 || row >= total_q) continue;
-    const int32_t id = block_table[(int64_t)r * max_blocks_per_seq + t / 16];
+  if (nq <= 0) return;
+  // window positions inside [0, 16 * max_blocks_per_seq)
+  const int64_t t0 = max((int64_t)L - nq, (int64_t)0);
+  const int64_t t1 = min((int64_t)L - 1, (int64_t)max_blocks_per_seq * 16 - 1);
+  const int runs = head_dim / 8;
+  for (int64_t blk = t0 / 16; blk <= t1 / 16 && t0 <= t1; ++blk) {
+    const int32_t id = block_table[(int64_t)r * max_blocks_per_seq + blk];
     if (id < 0 || id >= num_blocks) continue;   // an invalid id is not written
-    const int s = t % 16;
+    const int s_lo = (int)(max(t0, blk * 16) - blk * 16);
+    const int s_hi = (int)(min(t1, blk * 16 + 15) - blk * 16);
     const int64_t tile = ((int64_t)id * num_kv_heads + g) * head_dim * 16;
-    const int64_t src = ((int64_t)row * num_kv_heads + g) * head_dim + d;
-    k_pool[tile + ((d / 8) * 16 + s) * 8 + d % 8] = k_new[src];
-    v_pool[tile + (int64_t)d * 16 + s] = v_new[src];
+    // the window row of slot s (a row outside [0, total_q) leaves the slot)
+    auto row_of = [&](int s) -> int64_t {
+      const int64_t row = (int64_t)a + (blk * 16 + s) - ((int64_t)L - nq);
+      return row >= 0 && row < total_q ? row : -1;
+    };
+    if (tid < head_dim) {
+      uint16_t* vp = v_pool + tile + (int64_t)tid * 16;
+      Sector row = load_sector(vp);
+#pragma unroll
+      for (int s = 0; s < 16; ++s) {   // fixed indices keep the sector in registers
+        const int64_t q = s >= s_lo && s <= s_hi ? row_of(s) : -1;
+        if (q >= 0) row.e[s] = v_new[(q * num_kv_heads + g) * head_dim + tid];
+      }
+      store_sector(vp, row);
+    }
+    const int p_lo = s_lo / 2, np = s_hi / 2 - p_lo + 1;
+    if (tid < runs * np) {
+      const int c = tid % runs, pr = p_lo + tid / runs;
+      uint16_t* kp = k_pool + tile + (int64_t)(c * 16 + 2 * pr) * 8;
+      Sector run2 = load_sector(kp);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int s = 2 * pr + u;
+        const int64_t q = s >= s_lo && s <= s_hi ? row_of(s) : -1;
+        if (q < 0) continue;
+        const uint16_t* src = k_new + (q * num_kv_heads + g) * head_dim + c * 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) run2.e[u * 8 + e] = src[e];
+      }
+      store_sector(kp, run2);
+    }
   }
 }
 
@@ -74,6 +136,8 @@ extern "C" nsd_status nsd_kv_append(void* k_pool, void* v_pool, int64_t num_bloc
   if (bs == 0 || total_q == 0) return NSD_OK;
   if (!k_pool || !v_pool || !k_new || !v_new || !block_table || !seq_lens || !q_indptr)
     return fail(NSD_ERR_NULL, "%s: NULL pointer argument", fn);
+  if (((uintptr_t)k_pool | (uintptr_t)v_pool) % 16)
+    return fail(NSD_ERR_SHAPE, "%s: k_pool and v_pool must be 16-byte aligned", fn);
   clear_stale_error();
   hipLaunchKernelGGL(kv_append_kernel, dim3(num_kv_heads, bs), dim3(128), 0, (hipStream_t)stream,
                      (uint16_t*)k_pool, (uint16_t*)v_pool, (const uint16_t*)k_new,

@@ -138,6 +138,9 @@ def test_append_commit_alias_validation(lib):
     assert f(fake, fake, 8, fake, fake, fake, 0, fake, fake, 2, 8, 2, 16, 64, None) == 2   # no blocks
     assert f(None, None, 8, None, None, None, 4, None, None, 0, 8, 2, 16, 64, None) == 0   # bs == 0
     assert f(None, fake, 8, fake, fake, fake, 4, fake, fake, 2, 8, 2, 16, 64, None) == 1   # NULL
+    odd = ctypes.c_void_p(24)   # never dereferenced: refused before any launch
+    assert f(odd, fake, 8, fake, fake, fake, 4, fake, fake, 2, 8, 2, 16, 64, None) == 2    # alignment
+    assert b"16-byte aligned" in lib.nsd_last_error()
     g = lib.nsd_commit_lengths
     assert g(None, None, None, None, 0, None) == 0
     assert g(None, None, None, None, -1, None) == 2

@@ -36,6 +36,55 @@ def test_append_matches_oracle(device, cfg):
     assert np.array_equal(u16(kp), rk) and np.array_equal(u16(vp), rv)
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_append_edges_match_oracle(device, head_dim):
+    """Windows that cross a block boundary or span three blocks, block ids out
+    of range inside a window, positions past the table and contexts shorter
+    than the window.  The expected pools are the oracle's append applied token
+    by token to the tokens that have a position in the table and a valid
+    block id (the others are skipped); every other slot, including the rest
+    of each 32-byte sector the kernel rewrites, must keep its bytes."""
+    hkv, mbs, nb = 2, 4, 40
+    rng = np.random.default_rng(7)
+    # (seq_len, n_q, table row): block ids, -1 = invalid
+    cases = [(19, 5, [3, 4, -1, -1]),          # slots 14, 15 | 0, 1, 2 of the next block
+             (48, 40, [5, 6, 7, -1]),          # three blocks
+             (16, 1, [8, -1, -1, -1]),         # the last slot of a block
+             (33, 6, [9, -1, 10, -1]),         # the middle block invalid
+             (30, 4, [11, nb + 3, -1, -1]),    # an id past the pool
+             (70, 8, [12, 13, 14, 15]),        # positions past the table (64 slots)
+             (3, 5, [16, -1, -1, -1]),         # context shorter than the window
+             (1, 1, [17, -1, -1, -1])]
+    sl = np.array([c[0] for c in cases], dtype=np.int32)
+    nqs = np.array([c[1] for c in cases])
+    qi = np.concatenate([[0], np.cumsum(nqs)]).astype(np.int32)
+    bt = np.array([c[2] for c in cases], dtype=np.int32)
+    tq = int(qi[-1])
+    kp0 = torch.from_numpy(rng.integers(-30000, 30000, size=(nb, hkv, head_dim // 8, 16, 8),
+                                        dtype=np.int16)).view(torch.bfloat16)
+    vp0 = torch.from_numpy(rng.integers(-30000, 30000, size=(nb, hkv, head_dim, 16),
+                                        dtype=np.int16)).view(torch.bfloat16)
+    kn = torch.from_numpy(rng.integers(-30000, 30000, size=(tq, hkv, head_dim),
+                                       dtype=np.int16)).view(torch.bfloat16)
+    vn = torch.from_numpy(rng.integers(-30000, 30000, size=(tq, hkv, head_dim),
+                                       dtype=np.int16)).view(torch.bfloat16)
+    kp, vp = kp0.to(device), vp0.to(device)
+    nsd.kv_append(kp, vp, kn.to(device), vn.to(device), i32(bt, device), i32(sl, device),
+                  i32(qi, device))
+    torch.cuda.synchronize()
+    rk, rv = u16(kp0), u16(vp0)
+    for r, (L, nq, row) in enumerate(cases):
+        for j in range(nq):
+            t = L - nq + j
+            if t < 0 or t >= 16 * mbs or not 0 <= bt[r, t // 16] < nb:
+                continue
+            one = np.array([0, 1], dtype=np.int32)
+            rk, rv = oracle.commit.kv_append(rk, rv, u16(kn)[qi[r] + j:qi[r] + j + 1],
+                                             u16(vn)[qi[r] + j:qi[r] + j + 1], bt[r:r + 1],
+                                             np.array([t + 1]), one)
+    assert np.array_equal(u16(kp), rk) and np.array_equal(u16(vp), rv)
+
+
 def test_commit_lengths_matches_oracle(device):
     cfg = custom_config(seed=42, bs=50, k_lo=0, k_hi=8, pool_blocks=None, ctx_lo=20, ctx_hi=90)
     meta = make_meta(cfg)
