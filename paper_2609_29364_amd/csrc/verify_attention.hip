@@ -124,7 +124,7 @@ struct Params {
   const int32_t* seq_lens;
   const int32_t* q_indptr;
   uint16_t* out;
-  float* part_o;       // [4 * waves][MT*16][D]: head/tail partial O per range
+  uint16_t* part_o;    // [4 * waves][MT*16][D]: head/tail partial per range, O / sum in bf16
   float2* part_ml;     // [4 * waves][MT*16]: (running max, sum)
   struct CutRec* cut_rec;  // [2 * waves]: the item each range cuts at its end, for the merge
   uint32_t* prefix;    // [bs+1]: exclusive span prefix over the work order's positions
@@ -634,14 +634,14 @@ struct OutBuf {
 };
 
 constexpr int kOutO = 1;   // record of normalised bf16 output rows
-constexpr int kOutP = 2;   // record of fp32 partial rows (and their max, sum)
+constexpr int kOutP = 2;   // record of partial rows (normalised, bf16) and their fp32 max, sum
 
 // Bytes of one record (16-byte aligned): header, rows, and for partials each
 // row's (max, sum).
 template <int D>
 __host__ __device__ constexpr int out_record_bytes(int kind, int nrows) {
   return (kind == kOutO ? 16 + nrows * (D * 2 + 16)
-                        : 16 + nrows * (D * 4 + 16) + nrows * 8 + 15) / 16 * 16;
+                        : 16 + nrows * (D * 2 + 16) + nrows * 8 + 15) / 16 * 16;
 }
 
 // Ordering of the wave's LDS writes before its reads of other lanes' data,
@@ -678,13 +678,13 @@ __device__ inline void out_flush(const Params& p, OutBuf& ob, int lane) {
     } else {
       const int64_t slot = key;
       const int nr = nrows & 0xffff;
-      constexpr int RS = D * 4 + 16, CPR = D / 4, RPI = 64 / CPR;
+      constexpr int RS = D * 2 + 16, CPR = D / 8, RPI = 64 / CPR;
       const int c = lane % CPR, rr = lane / CPR;
       for (int r0 = 0; r0 < nr; r0 += RPI) {
         const int r = r0 + rr;
         if (r < nr)
-          *(f32x4*)(p.part_o + (slot * (MT * 16) + m0 + r) * D + c * 4) =
-              *(const f32x4*)(rows + r * RS + c * 16);
+          *(u32x4*)(p.part_o + (slot * (MT * 16) + m0 + r) * D + c * 8) =
+              *(const u32x4*)(rows + r * RS + c * 16);
       }
       if (lane < nr)
         p.part_ml[slot * (MT * 16) + m0 + lane] = *(const float2*)(rows + nr * RS + lane * 8);
@@ -720,22 +720,19 @@ __device__ inline void finish_item(const Params& p, Acc<D, MT>& a, const Item& i
                           : int4{kOutP, nr, mt * 16, slot};
     char* rows = rec + 16;
     if (row < nr) {
-      if (whole) {
-        const float inv = a.l[mt] > 0.f ? 1.f / a.l[mt] : 0.f;
+      // output rows, or a partial's rows over its own tokens (O / sum), in
+      // bf16; a partial also keeps the running max and sum that weight it in
+      // the merge
+      const float inv = a.l[mt] > 0.f ? 1.f / a.l[mt] : 0.f;
 #pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) {
-          const bf16x2 lo = {(__bf16)(a.o[mt][dt][0] * inv), (__bf16)(a.o[mt][dt][1] * inv)};
-          const bf16x2 hi = {(__bf16)(a.o[mt][dt][2] * inv), (__bf16)(a.o[mt][dt][3] * inv)};
-          *(u32x2*)(rows + row * (D * 2 + 16) + (dt * 16 + grp * 4) * 2) =
-              u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-        }
-      } else {
-#pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt)
-          *(f32x4*)(rows + row * (D * 4 + 16) + (dt * 16 + grp * 4) * 4) = a.o[mt][dt];
-        if (grp == 0)
-          *(float2*)(rows + nr * (D * 4 + 16) + row * 8) = make_float2(a.m[mt], a.l[mt]);
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const bf16x2 lo = {(__bf16)(a.o[mt][dt][0] * inv), (__bf16)(a.o[mt][dt][1] * inv)};
+        const bf16x2 hi = {(__bf16)(a.o[mt][dt][2] * inv), (__bf16)(a.o[mt][dt][3] * inv)};
+        *(u32x2*)(rows + row * (D * 2 + 16) + (dt * 16 + grp * 4) * 2) =
+            u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
       }
+      if (!whole && grp == 0)
+        *(float2*)(rows + nr * (D * 2 + 16) + row * 8) = make_float2(a.m[mt], a.l[mt]);
     }
     ob.used += need;
   }
@@ -1247,9 +1244,16 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
         const int64_t slot = s_slot[min(k0 + u, cnt - 1)];
         const int64_t row = slot * (MT * 16) + mld;
         ml[u] = p.part_ml[row];
-        const f32x4* src = (const f32x4*)(p.part_o + row * D) + c;
+        const u32x2* src = (const u32x2*)(p.part_o + row * D) + c;
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) o[u][i] = src[i * kTPR];
+        for (int i = 0; i < kPer; ++i) {
+          // bf16 to fp32 by placing each half in the high bits (exact); the
+          // compiler's conversion of bf16 vector elements read the low word
+          // for both halves here
+          const u32x2 w = src[i * kTPR];
+          o[u][i] = f32x4{__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                          __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)};
+        }
       }
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -1257,9 +1261,10 @@ __global__ __launch_bounds__(256) void combine_kernel(Params p) {
         const float mx = fmaxf(mrun, ml[u].x);
         const float a = mrun == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun - mx);
         const float b = __builtin_amdgcn_exp2f(ml[u].x - mx);
+        const float bl = b * ml[u].y;   // the part's weight: its rows are O / sum
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) orun[i] = a * orun[i] + b * o[u][i];
-        drun = a * drun + b * ml[u].y;
+        for (int i = 0; i < kPer; ++i) orun[i] = a * orun[i] + bl * o[u][i];
+        drun = a * drun + bl;
         mrun = mx;
       }
     }
@@ -1408,7 +1413,7 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool 
   // a head and a tail slot per range, W ranges in each of the two segments
   const size_t slots = 4 * (size_t)pl->num_waves * pl->mt * 16;
   pl->prefix_bytes = ((2 * ((size_t)bs + 1) + 2) * sizeof(uint32_t) + 255) / 256 * 256;
-  pl->part_o_bytes = slots * d * sizeof(float);
+  pl->part_o_bytes = slots * d * sizeof(uint16_t);
   pl->part_ml_bytes = slots * sizeof(float2);
   pl->cut_rec_bytes = 2 * (size_t)pl->num_waves * sizeof(CutRec);
   pl->ws_bytes = pl->prefix_bytes + pl->part_o_bytes + pl->part_ml_bytes + pl->cut_rec_bytes;
@@ -1505,7 +1510,7 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
   char* ws = (char*)workspace;
   p.prefix = (uint32_t*)ws;
   p.pos_of = p.prefix + bs + 1;
-  p.part_o = (float*)(ws + pl.prefix_bytes);
+  p.part_o = (uint16_t*)(ws + pl.prefix_bytes);
   p.part_ml = (float2*)(ws + pl.prefix_bytes + pl.part_o_bytes);
   p.cut_rec = (CutRec*)(ws + pl.prefix_bytes + pl.part_o_bytes + pl.part_ml_bytes);
   p.num_blocks = (int32_t)num_blocks;
