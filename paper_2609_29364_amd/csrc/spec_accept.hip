@@ -29,6 +29,7 @@
 // one 1 KiB chunk per row.
 #include "nsd_internal.h"
 
+#include <atomic>
 #include <mutex>
 
 namespace {
@@ -466,6 +467,27 @@ __global__ __launch_bounds__(kRowThreads) void accept_row_kernel(Args A) {
   pick_row<SAMPLE, kRowThreads>(A, r, a, k, n, s_sum, s_w, s_pre, s_c);
 }
 
+// CUs of the current device, queried once per device and kept (256 when the
+// device cannot be queried, which only picks the kernel layout).
+int device_cus() {
+  constexpr int kMaxDev = 64;
+  static std::atomic<int> cached[kMaxDev];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  int cus = cached[dev].load(std::memory_order_relaxed);
+  if (cus > 0) return cus;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  cached[dev].store(cus, std::memory_order_relaxed);
+  return cus;
+}
+
 int64_t sums_bytes(int64_t rows, int32_t vocab) {
   const int64_t nchunk = (vocab + kChunk - 1) / kChunk;
   return (rows * nchunk * 8 + 255) / 256 * 256;
@@ -486,13 +508,7 @@ nsd_status launch(bool sample, Args A, int32_t rows, void* workspace, size_t wor
   const dim3 g1((uint32_t)((A.nchunk + kSegChunks - 1) / kSegChunks) * (uint32_t)rows);
   // a batch with a row for every CU: one workgroup per row does both steps;
   // a smaller one spreads every row over several workgroups
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
-    (void)hipGetLastError();
-    cus = 256;
-  }
-  const bool one_pass = rows >= cus;
+  const bool one_pass = rows >= device_cus();
   clear_stale_error();
   if (one_pass) {
     if (sample)
