@@ -442,8 +442,13 @@ def kv_append(k_pool, v_pool, k_new, v_new, block_table, seq_lens, q_indptr):
     for t, n in ((block_table, "block_table"), (seq_lens, "seq_lens"), (q_indptr, "q_indptr")):
         _dev(t, torch.int32, n)
     total_q, hkv, d = k_new.shape
-    if v_new.shape != k_new.shape or k_pool.shape[1] != hkv:
+    nb = k_pool.shape[0]
+    if v_new.shape != k_new.shape or d % 8 or k_pool.shape != (nb, hkv, d // 8, BLOCK_SIZE, 8) \
+            or v_pool.shape != (nb, hkv, d, BLOCK_SIZE):
         raise ValueError("k_new/v_new must be [total_q][Hkv][D] matching the pools")
+    bs = seq_lens.numel()
+    if block_table.dim() != 2 or block_table.shape[0] != bs or q_indptr.numel() != bs + 1:
+        raise ValueError("block_table / q_indptr do not match seq_lens")
     _check("kv_append", lib().nsd_kv_append(
         _ptr(k_pool), _ptr(v_pool), k_pool.shape[0], _ptr(k_new), _ptr(v_new), _ptr(block_table),
         block_table.shape[1], _ptr(seq_lens), _ptr(q_indptr), seq_lens.numel(), total_q, hkv,
@@ -454,8 +459,15 @@ def commit_lengths(seq_lens, q_indptr, accepted_len, out=None):
     """Committed lengths seq_lens - K + accepted_len (int32 [bs])."""
     for t, n in ((seq_lens, "seq_lens"), (q_indptr, "q_indptr"), (accepted_len, "accepted_len")):
         _dev(t, torch.int32, n)
+    bs = seq_lens.numel()
+    if q_indptr.numel() != bs + 1 or accepted_len.numel() != bs:
+        raise ValueError("q_indptr / accepted_len do not match seq_lens")
     if out is None:
         out = torch.empty_like(seq_lens)
+    else:
+        _dev(out, torch.int32, "out")
+        if out.numel() != bs:
+            raise ValueError("out must have one entry per request")
     _check("commit_lengths", lib().nsd_commit_lengths(
         _ptr(seq_lens), _ptr(q_indptr), _ptr(accepted_len), _ptr(out), seq_lens.numel(),
         _stream(seq_lens)))

@@ -85,6 +85,29 @@ def test_append_edges_match_oracle(device, head_dim):
     assert np.array_equal(u16(kp), rk) and np.array_equal(u16(vp), rv)
 
 
+def test_append_and_commit_bindings_refuse_mismatched_shapes(device):
+    """The binding checks every shape the kernels index with before launching:
+    pools whose head_dim differs from the rows', a table of another batch
+    size, and a commit output of the wrong length are refused, and nothing
+    is written."""
+    bf = torch.bfloat16
+    kp = torch.zeros((8, 2, 64 // 8, 16, 8), dtype=bf, device=device)
+    vp = torch.zeros((8, 2, 64, 16), dtype=bf, device=device)
+    rows = torch.ones((3, 2, 128), dtype=bf, device=device)   # head_dim 128 against 64
+    bt = torch.zeros((2, 4), dtype=torch.int32, device=device)
+    sl = torch.tensor([3, 1], dtype=torch.int32, device=device)
+    qi = torch.tensor([0, 2, 3], dtype=torch.int32, device=device)
+    with pytest.raises(ValueError):
+        nsd.kv_append(kp, vp, rows, rows, bt, sl, qi)
+    rows64 = torch.ones((3, 2, 64), dtype=bf, device=device)
+    with pytest.raises(ValueError):
+        nsd.kv_append(kp, vp, rows64, rows64, bt[:1], sl, qi)
+    with pytest.raises(ValueError):
+        nsd.commit_lengths(sl, qi, sl, out=torch.empty(5, dtype=torch.int32, device=device))
+    torch.cuda.synchronize()
+    assert not kp.any() and not vp.any()
+
+
 def test_commit_lengths_matches_oracle(device):
     cfg = custom_config(seed=42, bs=50, k_lo=0, k_hi=8, pool_blocks=None, ctx_lo=20, ctx_hi=90)
     meta = make_meta(cfg)
