@@ -338,6 +338,8 @@ def spec_accept(p_target, q_draft, draft_tokens, uniforms, q_indptr, max_k, acce
         out_tokens = torch.empty(total_q, dtype=torch.int32, device=p_target.device)
     _dev(accepted_len, torch.int32, "accepted_len")
     _dev(out_tokens, torch.int32, "out_tokens")
+    if accepted_len.numel() != bs or out_tokens.numel() != total_q:
+        raise ValueError("accepted_len must have bs entries and out_tokens total_q")
     ws, ws_n = _accept_ws(workspace, bs, vocab, p_target.device)
     _check("spec_accept", lib().nsd_spec_accept(
         _ptr(p_target), _ptr(q_draft) if max_k > 0 else None,

@@ -104,6 +104,11 @@ def test_append_and_commit_bindings_refuse_mismatched_shapes(device):
         nsd.kv_append(kp, vp, rows64, rows64, bt[:1], sl, qi)
     with pytest.raises(ValueError):
         nsd.commit_lengths(sl, qi, sl, out=torch.empty(5, dtype=torch.int32, device=device))
+    p = torch.full((3, 8), 0.125, dtype=torch.float32, device=device)
+    u = torch.full((3,), 0.5, dtype=torch.float32, device=device)
+    with pytest.raises(ValueError):   # accepted_len shorter than the batch
+        nsd.spec_accept(p, p[:1], qi[:1], u, qi, 1,
+                        accepted_len=torch.empty(1, dtype=torch.int32, device=device))
     torch.cuda.synchronize()
     assert not kp.any() and not vp.any()
 
