@@ -149,7 +149,10 @@ int32_t    nsd_attention_waves(void);
  * Query j sits at position L_r - n_q + j and attends to tokens 0 .. L_r-n_q+j
  * of its request.  Query head h reads KV head h / (num_q_heads/num_kv_heads).
  *     out[q_indptr[r]+j][h] = softmax_t(scale * <q, k_t>) . v_t
- * computed from bf16 inputs with fp32 accumulation; out is rounded to bf16.
+ * computed from bf16 inputs with fp32 accumulation (the softmax weights enter
+ * the second product as bf16; a row split over several waves is merged from
+ * per-part rows stored normalised in bf16 with fp32 max and sum); out is
+ * rounded to bf16.
  * A query row with no visible token (only if n_q > L_r) is written as 0.
  *
  * q        : device, bf16 [total_q][num_q_heads][head_dim], total_q = q_indptr[bs].
