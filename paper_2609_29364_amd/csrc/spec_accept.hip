@@ -506,9 +506,10 @@ nsd_status launch(bool sample, Args A, int32_t rows, void* workspace, size_t wor
   A.ws_sum = (double*)workspace;
   A.ws_n = (int32_t*)((char*)workspace + sums_bytes(rows, A.vocab));
   const dim3 g1((uint32_t)((A.nchunk + kSegChunks - 1) / kSegChunks) * (uint32_t)rows);
-  // a batch with a row for every CU: one workgroup per row does both steps;
-  // a smaller one spreads every row over several workgroups
-  const bool one_pass = rows >= device_cus();
+  // a batch with a row for every CU, or rows of one segment each: one
+  // workgroup per row does both steps (a second launch would add nothing);
+  // otherwise every row is spread over several workgroups
+  const bool one_pass = rows >= device_cus() || A.nchunk <= kSegChunks;
   clear_stale_error();
   if (one_pass) {
     if (sample)
