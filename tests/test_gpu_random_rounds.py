@@ -17,7 +17,7 @@ from test_gpu_round_small import _check_all
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 120
+N_CASES = 400
 
 
 def _case(seed):
