@@ -110,7 +110,8 @@ __device__ inline bool request_rows(const Args& A, int r, int& a, int& k) {
 // when the request has no row (nothing to test or draw).
 template <bool SAMPLE>
 __device__ inline bool acceptance(const Args& A, int r, int lane, int wave, int& a, int& k,
-                                  int* s_n) {
+                                  int* s_n, int& x_lane) {
+  x_lane = -1;
   if (SAMPLE) {
     a = r;
     k = 0;
@@ -121,6 +122,7 @@ __device__ inline bool acceptance(const Args& A, int r, int lane, int wave, int&
     bool ok = true;
     if (lane < k) {
       const int x = A.x[a - r + lane];
+      x_lane = x;
       if (x < 0 || x >= A.vocab) {
         ok = false;
       } else {
@@ -252,8 +254,8 @@ __global__ __launch_bounds__(kThreads) void row_sums_kernel(Args A) {
   const int nseg = (A.nchunk + kSegChunks - 1) / kSegChunks;
   const int r = blockIdx.x / nseg;
   const int seg = blockIdx.x - r * nseg;
-  int a, k;
-  if (!acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n)) {
+  int a, k, x_lane;
+  if (!acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n, x_lane)) {
     if (seg == 0 && threadIdx.x == 0) A.ws_n[r] = 0;
     return;   // uniform over the workgroup: no row to stream
   }
@@ -272,141 +274,117 @@ __global__ __launch_bounds__(kThreads) void row_sums_kernel(Args A) {
   if (!SAMPLE && seg == 0 && threadIdx.x == 0) A.ws_n[r] = n;
 }
 
-// Exclusive scan of one value per thread over the NW waves of a workgroup;
-// *total gets the workgroup's sum.
-template <int NW>
-__device__ inline double block_excl_scan(double v, int lane, int wave, double* s_w,
-                                         double* total) {
-  const double incl = wave_incl_scan(v, lane);
-  double excl = __shfl_up(incl, 1);
-  if (lane == 0) excl = 0.0;
-  if (lane == 63) s_w[wave] = incl;
-  __syncthreads();
-  double off = 0.0, all = 0.0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    if (w < wave) off += s_w[w];
-    all += s_w[w];
-  }
-  *total = all;
-  __syncthreads();
-  return off + excl;
-}
-
 // The draw of request r (or sample row r) from its chunk sums s_sum[0,
-// nchunk), by a workgroup of NT threads: thread tid owns consecutive chunks,
-// a block scan of the thread totals finds the first chunk whose inclusive
-// prefix exceeds tau = u_K * S, and wave 0 scans inside that chunk.  Writes
-// the request's tokens and accepted length.
-template <bool SAMPLE, int NT>
-__device__ inline void pick_row(const Args& A, int r, int a, int k, int n, double* s_sum,
-                                double* s_w, double& s_pre, int& s_c) {
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+// nchunk), by one wave with no workgroup barrier: lane l owns consecutive
+// chunks and sums them, a wave scan gives every lane its prefix, the first
+// lane whose inclusive prefix exceeds tau = u_K * S finds its first chunk
+// whose inclusive prefix does (else the last chunk with mass is taken), and
+// the wave scans inside that chunk.  u_draw is u_K and x_lane this lane's
+// proposal token (lanes < K), both loaded early so their latency is hidden.
+// Writes the request's tokens and accepted length.
+template <bool SAMPLE>
+__device__ inline void draw_wave(const Args& A, int r, int a, int k, int n, double* s_sum,
+                                 float u_draw, int x_lane, int lane) {
   const int nchunk = A.nchunk;
   bool resid = n < k;
   const float* prow = row_p<SAMPLE>(A, r, a, n);
   const float* qrow = resid ? A.q + (int64_t)(a - r + n) * A.vocab : prow;
-  // thread tid owns chunks [c0, c1)
-  const int per = (nchunk + NT - 1) / NT;
-  const int c0 = min(nchunk, tid * per), c1 = min(nchunk, c0 + per);
-  double total = 0.0, pre = 0.0;
+  const int per = (nchunk + 63) / 64;
+  const int c0 = min(nchunk, lane * per), c1 = min(nchunk, c0 + per);
+  double local = 0.0, incl = 0.0, total = 0.0;
   for (int attempt = 0; attempt < 2; ++attempt) {
-    double local = 0.0;
+    local = 0.0;
     for (int c = c0; c < c1; ++c) local += s_sum[c];
-    pre = block_excl_scan<NT / 64>(local, lane, wave, s_w, &total);
+    incl = wave_incl_scan(local, lane);
+    total = __shfl(incl, 63);
     if (total > 0.0 || !resid) break;
-    // residual without mass: draw from p_n itself
+    // residual without mass: draw from p_n itself (its sums, by this wave)
     resid = false;
     qrow = prow;
-    chunk_sums<NT / 64>(prow, qrow, false, A.vocab, 0, nchunk, lane, wave, s_sum);
-    __syncthreads();
+    chunk_sums<1>(prow, qrow, false, A.vocab, 0, nchunk, lane, 0, s_sum);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's sums are in LDS
   }
-  const double tau = (double)A.u[a + k] * total;
-  int y = -1;
+  double excl = __shfl_up(incl, 1);
+  if (lane == 0) excl = 0.0;
+  const double tau = (double)u_draw * total;
+  int cstar = -1;
+  double cpre = 0.0;
   if (total > 0.0) {
-    // the first chunk whose inclusive prefix exceeds tau, else the last with mass
-    if (tid == 0) s_c = 0x7fffffff;
-    __syncthreads();
-    double run = pre;
-    int found = -1;
-    double found_pre = 0.0;
+    // each lane's first chunk whose inclusive prefix exceeds tau, and its last
+    // chunk with mass; the first lane with such a chunk gives it, else
+    // (rounding left tau at or past the total) the last lane with mass does
+    int found = -1, last = -1;
+    double fpre = 0.0, lpre = 0.0, run = excl;
     for (int c = c0; c < c1; ++c) {
-      if (run + s_sum[c] > tau) {
+      const double v = s_sum[c];
+      if (found < 0 && run + v > tau) {
         found = c;
-        found_pre = run;
-        break;
+        fpre = run;
       }
-      run += s_sum[c];
+      if (v > 0.0) {
+        last = c;
+        lpre = run;
+      }
+      run += v;
     }
-    if (found >= 0) atomicMin(&s_c, found);
-    __syncthreads();
-    if (found >= 0 && found == s_c) s_pre = found_pre;
-    if (s_c == 0x7fffffff) {
-      __syncthreads();
-      if (tid == 0) s_c = -1;
-      __syncthreads();
-      int last = -1;
-      double last_pre = 0.0, acc = pre;
-      for (int c = c0; c < c1; ++c) {
-        if (s_sum[c] > 0.0) {
-          last = c;
-          last_pre = acc;
-        }
-        acc += s_sum[c];
-      }
-      if (last >= 0) atomicMax(&s_c, last);
-      __syncthreads();
-      if (last >= 0 && last == s_c) s_pre = last_pre;
-    }
-    __syncthreads();
-    // scan inside the chosen chunk (wave 0)
-    if (wave == 0) {
-      const int cstar = max(s_c, 0);   // s_c >= 0 whenever total > 0
-      const int idx = cstar * kChunk + lane * 4;
-      f32x4 pv = (f32x4){0.f, 0.f, 0.f, 0.f}, qv = pv;
-      if (idx < A.vocab) {
-        pv = *(const f32x4*)(prow + idx);
-        if (resid) qv = *(const f32x4*)(qrow + idx);
-      }
-      double w[4];
-      weights4(pv, qv, resid, w);
-      const double ls = ((w[0] + w[1]) + w[2]) + w[3];
-      const double incl = wave_incl_scan(ls, lane);
-      double rr = __shfl_up(incl, 1);
-      if (lane == 0) rr = 0.0;
-      rr += s_pre;
-      int f = -1, last_pos = -1;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        rr += w[e];
-        if (w[e] > 0.0) {
-          last_pos = e;
-          if (f < 0 && rr > tau) f = e;
-        }
-      }
-      const uint64_t fm = __ballot(f >= 0);
-      if (fm) {
-        const int fl = __ffsll((unsigned long long)fm) - 1;
-        y = cstar * kChunk + fl * 4 + __shfl(f, fl);
-      } else {
-        const uint64_t pm = __ballot(last_pos >= 0);
-        if (pm) {
-          const int pl = 63 - __clzll((long long)pm);
-          y = cstar * kChunk + pl * 4 + __shfl(last_pos, pl);
-        }
+    const uint64_t over = __ballot(found >= 0);
+    if (over) {
+      const int owner = __ffsll((unsigned long long)over) - 1;
+      cstar = __shfl(found, owner);
+      cpre = __shfl(fpre, owner);
+    } else {
+      const uint64_t has = __ballot(last >= 0);
+      if (has) {
+        const int owner = 63 - __clzll((long long)has);
+        cstar = __shfl(last, owner);
+        cpre = __shfl(lpre, owner);
       }
     }
   }
-  if (wave != 0) return;
+  int y = -1;
+  if (cstar >= 0) {
+    // scan inside the chosen chunk
+    const int idx = cstar * kChunk + lane * 4;
+    f32x4 pv = (f32x4){0.f, 0.f, 0.f, 0.f}, qv = pv;
+    if (idx < A.vocab) {
+      pv = *(const f32x4*)(prow + idx);
+      if (resid) qv = *(const f32x4*)(qrow + idx);
+    }
+    double w[4];
+    weights4(pv, qv, resid, w);
+    const double ls = ((w[0] + w[1]) + w[2]) + w[3];
+    const double inc = wave_incl_scan(ls, lane);
+    double rr = __shfl_up(inc, 1);
+    if (lane == 0) rr = 0.0;
+    rr += cpre;
+    int f = -1, last_pos = -1;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      rr += w[e];
+      if (w[e] > 0.0) {
+        last_pos = e;
+        if (f < 0 && rr > tau) f = e;
+      }
+    }
+    const uint64_t fm = __ballot(f >= 0);
+    if (fm) {
+      const int fl = __ffsll((unsigned long long)fm) - 1;
+      y = cstar * kChunk + fl * 4 + __shfl(f, fl);
+    } else {
+      const uint64_t pm = __ballot(last_pos >= 0);
+      if (pm) {
+        const int pl = 63 - __clzll((long long)pm);
+        y = cstar * kChunk + pl * 4 + __shfl(last_pos, pl);
+      }
+    }
+  }
   if (SAMPLE) {
     if (lane == 0) A.out_tokens[(int64_t)r * A.out_stride] = y;
     return;
   }
   if (lane <= k) {
     int tok = -1;
-    if (lane < n) tok = A.x[a - r + lane];
+    if (lane < n) tok = x_lane;
     else if (lane == n) tok = y;
     A.out_tokens[a + lane] = tok;
   }
@@ -416,23 +394,24 @@ __device__ inline void pick_row(const Args& A, int r, int a, int k, int n, doubl
 template <bool SAMPLE>
 __global__ __launch_bounds__(kThreads) void pick_kernel(Args A) {
   __shared__ double s_sum[kMaxChunks];
-  __shared__ double s_w[kWaves];
-  __shared__ double s_pre;
-  __shared__ int s_c;
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
   const int r = blockIdx.x;
-  int a = r, k = 0, n = 0;
+  int a = r, k = 0, n = 0, x_lane = -1;
   if (!SAMPLE) {
     if (!request_rows(A, r, a, k)) {
       if (tid == 0) A.accepted_len[r] = 0;
       return;
     }
     n = min(max(A.ws_n[r], 0), k);
+    if (tid < k) x_lane = A.x[a - r + tid];
   }
+  const float u_draw = A.u[a + k];
   const double* sums = A.ws_sum + (int64_t)r * A.nchunk;
   for (int c = tid; c < A.nchunk; c += kThreads) s_sum[c] = sums[c];
   __syncthreads();
-  pick_row<SAMPLE, kThreads>(A, r, a, k, n, s_sum, s_w, s_pre, s_c);
+  if (tid >= 64) return;
+  draw_wave<SAMPLE>(A, r, a, k, n, s_sum, u_draw, x_lane, lane);
 }
 
 // Both steps for one row per workgroup of kRowThreads threads (used when the
@@ -442,15 +421,12 @@ __global__ __launch_bounds__(kThreads) void pick_kernel(Args A) {
 template <bool SAMPLE>
 __global__ __launch_bounds__(kRowThreads) void accept_row_kernel(Args A) {
   __shared__ double s_sum[kMaxChunks];
-  __shared__ double s_w[kRowThreads / 64];
-  __shared__ double s_pre;
-  __shared__ int s_c;
   __shared__ int s_n;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = blockIdx.x;
-  int a, k;
-  if (!acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n)) {
+  int a, k, x_lane;
+  if (!acceptance<SAMPLE>(A, r, lane, wave, a, k, &s_n, x_lane)) {
     if (threadIdx.x == 0) A.accepted_len[r] = 0;
     return;
   }
@@ -462,9 +438,11 @@ __global__ __launch_bounds__(kRowThreads) void accept_row_kernel(Args A) {
   const bool resid = n < k;
   const float* prow = row_p<SAMPLE>(A, r, a, n);
   const float* qrow = resid ? A.q + (int64_t)(a - r + n) * A.vocab : prow;
+  const float u_draw = wave == 0 ? A.u[a + k] : 0.f;   // in flight while the row streams
   chunk_sums<kRowThreads / 64>(prow, qrow, resid, A.vocab, 0, A.nchunk, lane, wave, s_sum);
   __syncthreads();
-  pick_row<SAMPLE, kRowThreads>(A, r, a, k, n, s_sum, s_w, s_pre, s_c);
+  if (wave != 0) return;
+  draw_wave<SAMPLE>(A, r, a, k, n, s_sum, u_draw, x_lane, lane);
 }
 
 // CUs of the current device, queried once per device and kept (256 when the
