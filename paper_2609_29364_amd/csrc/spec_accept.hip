@@ -6,8 +6,8 @@
 // A request's weight row (max(0, p_n - q_n) after a rejection at n, or the
 // bonus row p_K) is 151936 floats in the workloads: streaming it is the whole
 // cost.  A batch with a row for every CU runs accept_row_kernel: one
-// 1024-thread workgroup per row takes the acceptance tests, streams the row
-// into chunk sums held in LDS, and draws, in one launch.  A smaller batch
+// 256-thread workgroup per row takes the acceptance tests, streams the row
+// into chunk sums held in LDS, and draws with one wave, in one launch.  A smaller batch
 // spreads each row over several workgroups, in two kernels:
 //
 // 1. row_sums_kernel, one 256-thread workgroup per (row, segment of 64
@@ -19,11 +19,11 @@
 //    reduced together in one butterfly) and writes each chunk's fp64 sum to
 //    the workspace.  The row is spread over
 //    the whole chip instead of one workgroup per request.
-// 2. pick_kernel, one 256-thread workgroup per row: reads the row's chunk sums,
-//    scans them (a thread owns consecutive chunks; a block scan of the thread
-//    totals), finds the first chunk whose inclusive prefix exceeds
-//    tau = u_K * S, re-reads that one chunk and picks the first token t with
-//    w(t) > 0 whose running prefix exceeds tau.  A residual without mass (only
+// 2. pick_kernel, one 256-thread workgroup per row: loads the row's chunk
+//    sums into LDS; one wave scans them (a lane owns consecutive chunks; a
+//    wave scan of the lane totals), finds the first chunk whose inclusive
+//    prefix exceeds tau = u_K * S, re-reads that one chunk and picks the
+//    first token t with w(t) > 0 whose running prefix exceeds tau.  A residual without mass (only
 //    possible through fp32 rounding) falls back to p_n, streamed here.
 // Traffic: each needed row once, plus the chunk sums (8 bytes per 1 KiB) and
 // one 1 KiB chunk per row.
@@ -40,7 +40,7 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 256;       // weights per chunk: 64 lanes x 4
 constexpr int kUnroll = 4;
-constexpr int kRowThreads = 1024;   // accept_row_kernel: 16 waves per row
+constexpr int kRowThreads = 256;   // accept_row_kernel: 4 waves per row
 constexpr int kSegChunks = kWaves * kUnroll * 4;   // chunks per row_sums workgroup
 constexpr int kMaxVocab = 1 << 19;
 constexpr int kMaxChunks = kMaxVocab / kChunk;
@@ -64,14 +64,47 @@ struct Args {
   int32_t* out_tokens;
 };
 
-// Inclusive prefix sum across the wave (Hillis-Steele).
-__device__ inline double wave_incl_scan(double x, int lane) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  return x;
+// Lane l's view of x in lane src(l) under a DPP control (row_mask and
+// bank_mask select the lanes that take it; the others, and lanes whose source
+// is outside the row or wave, get 0).  fp64 moves as two 32-bit DPP moves.
+template <int CTRL, int ROW_MASK, int BANK_MASK>
+__device__ __attribute__((always_inline)) inline double dpp_f64(double x) {
+  const uint64_t b = (uint64_t)__double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROW_MASK, BANK_MASK, true);
+  const int hi =
+      __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, ROW_MASK, BANK_MASK, true);
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+
+// Inclusive prefix sum across the wave with DPP lane moves: within each row
+// of 16 lanes the sums of 4 (shifts by 1, 2 and 3), then 8 and 16 (shifts by
+// 4 and 8 into the upper banks), then the row totals carried across rows
+// (broadcasts of lanes 15 and 31).
+__device__ __attribute__((always_inline)) inline double wave_incl_scan(double v) {
+  double s = v + dpp_f64<0x111, 0xf, 0xf>(v);   // row_shr:1
+  s += dpp_f64<0x112, 0xf, 0xf>(v);             // row_shr:2
+  s += dpp_f64<0x113, 0xf, 0xf>(v);             // row_shr:3
+  s += dpp_f64<0x114, 0xf, 0xe>(s);             // row_shr:4, banks 1-3
+  s += dpp_f64<0x118, 0xf, 0xc>(s);             // row_shr:8, banks 2-3
+  s += dpp_f64<0x142, 0xa, 0xf>(s);             // row_bcast:15, rows 1 and 3
+  s += dpp_f64<0x143, 0xc, 0xf>(s);             // row_bcast:31, rows 2 and 3
+  return s;
+}
+
+// Lane l's value in every lane; l must be the same in all lanes.
+__device__ __attribute__((always_inline)) inline int lane_value(int v, int l) {
+  return __builtin_amdgcn_readlane(v, l);
+}
+__device__ __attribute__((always_inline)) inline double lane_value(double v, int l) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)b, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// The previous lane's value (0 in lane 0): DPP wave_shr:1.
+__device__ __attribute__((always_inline)) inline double wave_prev(double v) {
+  return dpp_f64<0x138, 0xf, 0xf>(v);
 }
 
 __device__ inline void weights4(const f32x4& pv, const f32x4& qv, bool resid, double w[4]) {
@@ -142,24 +175,22 @@ __device__ inline const float* row_p(const Args& A, int r, int a, int n) {
   return SAMPLE ? A.p + (int64_t)r * A.row_stride : A.p + (int64_t)(a + n) * A.vocab;
 }
 
-// One iteration's loads: chunks c0 + u * NW (u < kUnroll) of the weight row,
-// one 16-byte load per lane and chunk (and the draft row's with RESID).
-// Without CHECK every chunk must be whole and inside [., c_end); with it,
-// chunks past c_end and elements past the vocabulary read as zero.
+// One iteration's loads: chunks c0 + u * NW (u < kUnroll) of the weight row, one
+// 16-byte load per lane and chunk (and the draft row's with RESID).  Without
+// CHECK every chunk must be whole and inside [., c_end); with it, chunks past
+// c_end load chunk c_end - 1 again and lanes past the vocabulary its last four
+// weights, so every load is unconditional and in bounds (the reduction drops
+// both).
 template <bool RESID, bool CHECK, int NW>
 __device__ __attribute__((always_inline)) inline void load_chunks(const float* prow, const float* qrow, int vocab, int c0,
                                    int c_end, int lane, f32x4 (&pv)[kUnroll],
                                    f32x4 (&qv)[kUnroll]) {
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
-    const int c = c0 + u * NW;
-    const int idx = c * kChunk + lane * 4;
-    pv[u] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    qv[u] = pv[u];
-    if (!CHECK || (c < c_end && idx < vocab)) {
-      pv[u] = __builtin_nontemporal_load((const f32x4*)(prow + idx));
-      if (RESID) qv[u] = __builtin_nontemporal_load((const f32x4*)(qrow + idx));
-    }
+    const int c = CHECK ? min(c0 + u * NW, c_end - 1) : c0 + u * NW;
+    const int idx = CHECK ? min(c * kChunk + lane * 4, vocab - 4) : c * kChunk + lane * 4;
+    pv[u] = __builtin_nontemporal_load((const f32x4*)(prow + idx));
+    qv[u] = RESID ? __builtin_nontemporal_load((const f32x4*)(qrow + idx)) : pv[u];
   }
   // keep the reduction of the previous iteration after these loads: they go
   // out first, so the wave always has an iteration's loads in flight
@@ -168,16 +199,18 @@ __device__ __attribute__((always_inline)) inline void load_chunks(const float* p
 
 // The four chunk sums of one iteration in one butterfly, into dst: halves of
 // the lanes swap two chunks' values (xor 32), then one (xor 16), then 16-lane
-// sums; lanes 0, 16, 32, 48 end with chunks 0, 1, 2, 3.
-template <bool RESID, int NW>
+// sums; lanes 0, 16, 32, 48 end with chunks 0, 1, 2, 3.  Chunks past c_end
+// are not stored; with CHECK, lanes past the vocabulary count zero.
+template <bool RESID, bool CHECK, int NW>
 __device__ __attribute__((always_inline)) inline void reduce_chunks(const f32x4 (&pv)[kUnroll], const f32x4 (&qv)[kUnroll],
-                                     int c0, int c_end, int lane, double* dst) {
+                                     int c0, int c_end, int vocab, int lane, double* dst) {
   double v[kUnroll];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
     double w[4];
     weights4(pv[u], qv[u], RESID, w);
     v[u] = ((w[0] + w[1]) + w[2]) + w[3];
+    if (CHECK && (c0 + u * NW) * kChunk + lane * 4 >= vocab) v[u] = 0.0;
   }
   const bool h5 = lane & 32, h4 = lane & 16;
   const double r0 = (h5 ? v[2] : v[0]) + __shfl_xor(h5 ? v[0] : v[2], 32);
@@ -190,6 +223,7 @@ __device__ __attribute__((always_inline)) inline void reduce_chunks(const f32x4 
     if (c < c_end) dst[c] = s;
   }
 }
+static_assert(kUnroll == 4, "the butterfly in reduce_chunks reduces four chunks");
 
 // Sums of chunks [c_beg, c_end) of the weight row into dst[c], by the NW
 // waves of a workgroup: wave w takes iterations of kUnroll chunks w, w + NW,
@@ -197,8 +231,8 @@ __device__ __attribute__((always_inline)) inline void reduce_chunks(const f32x4 
 // iteration's loads in flight while it reduces the current one.  Every
 // iteration but a wave's last covers whole chunks inside the range (only the
 // range's last chunk can be partial, and it falls in the last iteration of
-// the wave holding it), so the loop's loads are unconditional; the last
-// iteration's are checked.
+// the wave holding it), so the loop's loads need no checks; the last
+// iteration's addresses are clamped into the range.
 template <int NW, bool RESID>
 __device__ __attribute__((always_inline)) inline void chunk_sums_t(const float* prow, const float* qrow, int vocab, int c_beg,
                                     int c_end, int lane, int wave, double* dst) {
@@ -209,7 +243,7 @@ __device__ __attribute__((always_inline)) inline void chunk_sums_t(const float* 
   f32x4 pa[kUnroll], qa[kUnroll], pb[kUnroll], qb[kUnroll];
   if (n_iter == 1) {
     load_chunks<RESID, true, NW>(prow, qrow, vocab, first, c_end, lane, pa, qa);
-    reduce_chunks<RESID, NW>(pa, qa, first, c_end, lane, dst);
+    reduce_chunks<RESID, true, NW>(pa, qa, first, c_end, vocab, lane, dst);
     return;
   }
   // two register sets used in turn (unrolled by two, so no set is copied: a
@@ -218,21 +252,21 @@ __device__ __attribute__((always_inline)) inline void chunk_sums_t(const float* 
   int c0 = first, it = 0;
   for (; it + 3 < n_iter; it += 2, c0 += 2 * kStep) {
     load_chunks<RESID, false, NW>(prow, qrow, vocab, c0 + kStep, c_end, lane, pb, qb);
-    reduce_chunks<RESID, NW>(pa, qa, c0, c_end, lane, dst);
+    reduce_chunks<RESID, false, NW>(pa, qa, c0, c_end, vocab, lane, dst);
     load_chunks<RESID, false, NW>(prow, qrow, vocab, c0 + 2 * kStep, c_end, lane, pa, qa);
-    reduce_chunks<RESID, NW>(pb, qb, c0 + kStep, c_end, lane, dst);
+    reduce_chunks<RESID, false, NW>(pb, qb, c0 + kStep, c_end, vocab, lane, dst);
   }
   // two or three iterations left, the first of them loaded
   if (n_iter - it == 3) {
     load_chunks<RESID, false, NW>(prow, qrow, vocab, c0 + kStep, c_end, lane, pb, qb);
-    reduce_chunks<RESID, NW>(pa, qa, c0, c_end, lane, dst);
+    reduce_chunks<RESID, false, NW>(pa, qa, c0, c_end, vocab, lane, dst);
     load_chunks<RESID, true, NW>(prow, qrow, vocab, c0 + 2 * kStep, c_end, lane, pa, qa);
-    reduce_chunks<RESID, NW>(pb, qb, c0 + kStep, c_end, lane, dst);
-    reduce_chunks<RESID, NW>(pa, qa, c0 + 2 * kStep, c_end, lane, dst);
+    reduce_chunks<RESID, false, NW>(pb, qb, c0 + kStep, c_end, vocab, lane, dst);
+    reduce_chunks<RESID, true, NW>(pa, qa, c0 + 2 * kStep, c_end, vocab, lane, dst);
   } else {
     load_chunks<RESID, true, NW>(prow, qrow, vocab, c0 + kStep, c_end, lane, pb, qb);
-    reduce_chunks<RESID, NW>(pa, qa, c0, c_end, lane, dst);
-    reduce_chunks<RESID, NW>(pb, qb, c0 + kStep, c_end, lane, dst);
+    reduce_chunks<RESID, false, NW>(pa, qa, c0, c_end, vocab, lane, dst);
+    reduce_chunks<RESID, true, NW>(pb, qb, c0 + kStep, c_end, vocab, lane, dst);
   }
 }
 
@@ -244,7 +278,6 @@ __device__ __attribute__((always_inline)) inline void chunk_sums(const float* pr
   else
     chunk_sums_t<NW, false>(prow, qrow, vocab, c_beg, c_end, lane, wave, dst);
 }
-static_assert(kUnroll == 4, "the butterfly in chunk_sums reduces four chunks");
 
 template <bool SAMPLE>
 __global__ __launch_bounds__(kThreads) void row_sums_kernel(Args A) {
@@ -295,8 +328,8 @@ __device__ inline void draw_wave(const Args& A, int r, int a, int k, int n, doub
   for (int attempt = 0; attempt < 2; ++attempt) {
     local = 0.0;
     for (int c = c0; c < c1; ++c) local += s_sum[c];
-    incl = wave_incl_scan(local, lane);
-    total = __shfl(incl, 63);
+    incl = wave_incl_scan(local);
+    total = lane_value(incl, 63);
     if (total > 0.0 || !resid) break;
     // residual without mass: draw from p_n itself (its sums, by this wave)
     resid = false;
@@ -304,8 +337,7 @@ __device__ inline void draw_wave(const Args& A, int r, int a, int k, int n, doub
     chunk_sums<1>(prow, qrow, false, A.vocab, 0, nchunk, lane, 0, s_sum);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's sums are in LDS
   }
-  double excl = __shfl_up(incl, 1);
-  if (lane == 0) excl = 0.0;
+  const double excl = wave_prev(incl);
   const double tau = (double)u_draw * total;
   int cstar = -1;
   double cpre = 0.0;
@@ -330,14 +362,14 @@ __device__ inline void draw_wave(const Args& A, int r, int a, int k, int n, doub
     const uint64_t over = __ballot(found >= 0);
     if (over) {
       const int owner = __ffsll((unsigned long long)over) - 1;
-      cstar = __shfl(found, owner);
-      cpre = __shfl(fpre, owner);
+      cstar = lane_value(found, owner);
+      cpre = lane_value(fpre, owner);
     } else {
       const uint64_t has = __ballot(last >= 0);
       if (has) {
         const int owner = 63 - __clzll((long long)has);
-        cstar = __shfl(last, owner);
-        cpre = __shfl(lpre, owner);
+        cstar = lane_value(last, owner);
+        cpre = lane_value(lpre, owner);
       }
     }
   }
@@ -353,10 +385,7 @@ __device__ inline void draw_wave(const Args& A, int r, int a, int k, int n, doub
     double w[4];
     weights4(pv, qv, resid, w);
     const double ls = ((w[0] + w[1]) + w[2]) + w[3];
-    const double inc = wave_incl_scan(ls, lane);
-    double rr = __shfl_up(inc, 1);
-    if (lane == 0) rr = 0.0;
-    rr += cpre;
+    double rr = wave_prev(wave_incl_scan(ls)) + cpre;
     int f = -1, last_pos = -1;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -369,12 +398,12 @@ __device__ inline void draw_wave(const Args& A, int r, int a, int k, int n, doub
     const uint64_t fm = __ballot(f >= 0);
     if (fm) {
       const int fl = __ffsll((unsigned long long)fm) - 1;
-      y = cstar * kChunk + fl * 4 + __shfl(f, fl);
+      y = cstar * kChunk + fl * 4 + lane_value(f, fl);
     } else {
       const uint64_t pm = __ballot(last_pos >= 0);
       if (pm) {
         const int pl = 63 - __clzll((long long)pm);
-        y = cstar * kChunk + pl * 4 + __shfl(last_pos, pl);
+        y = cstar * kChunk + pl * 4 + lane_value(last_pos, pl);
       }
     }
   }
