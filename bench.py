@@ -37,7 +37,8 @@ def parse():
                     help="kv_gather and verify_attention as separate kernels")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--ceiling", action="store_true",
-                    help="only the HBM probe: the fused pass's read/write mix on verify_8b with "
+                    help="only the HBM probe: one layer's fused-pass read/write mix on the workload "
+                         "(verify_8b unless --workload names another), with "
                          "the written tiles placed four ways (gathered at the end of every "
                          "wave's sequence, spread through it, on a share of the waves, or "
                          "stored by waves that do not read), and the writes alone")
@@ -985,11 +986,13 @@ def ceiling_bench(args):
     cfg = CONFIGS[args.workload]
     meta = make_meta(cfg)
     alg = algorithmic_bytes(cfg, meta)
-    w = alg["gather"] // 2
-    res = {"mode": "ceiling", "workload": cfg.name, "read_bytes": alg["fused"] - w,
-           "write_bytes": w}
+    # one layer's pass (a many-layer round runs the same pass once per layer)
+    layers = cfg.num_layers
+    w = alg["gather"] // 2 // layers
+    res = {"mode": "ceiling", "workload": cfg.name, "layers": layers,
+           "read_bytes": alg["fused"] // layers - w, "write_bytes": w}
     for placement in ("end", "spread", "waves", "writer"):
-        res[placement] = practical_ceiling(dev, alg["fused"] - w, w, placement=placement)
+        res[placement] = practical_ceiling(dev, res["read_bytes"], w, placement=placement)
     print(json.dumps(res), flush=True)
 
 
@@ -1044,17 +1047,31 @@ def sweep_bench(args):
             if cfg.num_layers > 1:
                 torch.cuda.empty_cache()
         acc_in = make_accept(cfg, meta, dev)
-        acc_ms, acc_host = 0.0, None
+        acc_ms, acc_host, acc_cold_ms = 0.0, None, None
         if acc_in is not None:
             al = torch.empty(cfg.bs, dtype=torch.int32, device=dev)
             tk = torch.empty(meta.total_q, dtype=torch.int32, device=dev)
             aw = torch.empty(nsd.accept_workspace_size(cfg.bs, cfg.vocab), dtype=torch.uint8,
                              device=dev)
-            acc_ms = timed(lambda: nsd.spec_accept(
+            accept = lambda: nsd.spec_accept(
                 acc_in.p_target, acc_in.q_draft, acc_in.draft_tokens, acc_in.uniforms, qi,
-                int(meta.depth.max()), accepted_len=al, out_tokens=tk, workspace=aw),
-                args.warmup, args.steps)
+                int(meta.depth.max()), accepted_len=al, out_tokens=tk, workspace=aw)
+            acc_ms = timed(accept, args.warmup, args.steps)
             acc_host = al.cpu().numpy()
+            # each call after a 1 GiB read, so none of its rows is left in the
+            # infinity cache (as inside a round, after the attention passes)
+            scrub = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+            sink = torch.empty((), dtype=torch.float32, device=dev)
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(args.steps)]
+            for a, b in ev:
+                torch.sum(scrub, dim=0, out=sink)
+                a.record(stream)
+                accept()
+                b.record(stream)
+            torch.cuda.synchronize()
+            acc_cold_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+            del scrub, sink
         alg = algorithmic_bytes(cfg, meta, acc_host)
         fused_ms = float(np.sum(layer_ms))
         round_ms = fused_ms + acc_ms
@@ -1070,8 +1087,18 @@ def sweep_bench(args):
                                              (fused_ms * 1e-3) / 1e12, 3),
                "accept_tbs": (round(alg["accept"] / (acc_ms * 1e-3) / 1e12, 3)
                               if acc_ms > 0 else None),
+               "accept_scrubbed_ms": (round(acc_cold_ms, 4) if acc_cold_ms else None),
+               "accept_scrubbed_tbs": (round(alg["accept"] / (acc_cold_ms * 1e-3) / 1e12, 3)
+                                       if acc_cold_ms else None),
                "timing": f"mean of {reps} back-to-back passes per layer after {args.warmup} "
                          f"warm-up, HIP events on the launching stream"}
+        if name != "tiny" and not args.no_ceiling:
+            # the probe on one layer's read/write mix (the tiny round is cache-resident)
+            wb = alg["gather"] // 2 // cfg.num_layers
+            c = practical_ceiling(dev, alg["fused"] // cfg.num_layers - wb, wb)
+            res["probe_mix_gbs"] = c["mix_gbs"]
+            res["probe_read_only_gbs"] = c["read_only_gbs"]
+            res["fused_of_probe"] = round(alg["fused"] / (fused_ms * 1e-3) / 1e9 / c["mix_gbs"], 4)
         if lay0 is not None:
             res["cpu_baseline"] = cpu_baseline(cfg, meta, lay0, acc_in, args.cpu_seconds)
         print(json.dumps(res), flush=True)
