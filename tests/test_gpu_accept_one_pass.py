@@ -1,7 +1,8 @@
 """The one-launch acceptance and sampling kernel (a workgroup per row, used
 once a batch has a row for every CU) at the vocabulary sizes where its
 one-wave draw gives each lane the longest run of chunk sums (2^19 weights:
-32 chunks per lane), against the oracle."""
+32 chunks per lane), and the empty-residual fallback of both acceptance
+paths over many chunks, against the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -51,3 +52,26 @@ def test_accept_one_launch_at_the_largest_vocabulary(device):
     # both outcomes occur: rejections (residual rows) and full acceptances (bonus rows)
     n = al.cpu().numpy()
     assert (n < meta.depth).any() and (n == meta.depth).any()
+
+
+@pytest.mark.parametrize("bs", [6, ROWS])
+def test_empty_residual_draws_from_the_target_row(device, bs):
+    # every proposal lies outside the vocabulary (rejected) and q_0 = p_0, so
+    # every residual is empty and the token is drawn from p_0 itself; 16388
+    # weights are 65 chunks (more than one per lane of the one-wave draw), so
+    # 6 requests take the two-kernel path and ROWS the one-launch kernel
+    vocab = 16388
+    g = torch.Generator(device=device).manual_seed(bs)
+    q_indptr = np.arange(0, 2 * bs + 1, 2, dtype=np.int32)
+    p = torch.rand(2 * bs, vocab, generator=g, device=device) ** 4
+    p[0, :] = 0.0
+    p[0, vocab - 3] = 1.0                               # a one-token target row
+    q = p[0::2].contiguous()                            # q_0 = p_0 exactly
+    x = torch.full((bs,), vocab + 5, dtype=torch.int32, device=device)
+    u = (torch.randint(0, 1 << 24, (2 * bs,), generator=g, device=device) * 2.0**-24).float()
+    acc, tok = nsd.spec_accept(p, q, x, u, i32(q_indptr, device), 1)
+    torch.cuda.synchronize()
+    acc, tok = acc.cpu().numpy(), tok.cpu().numpy()
+    assert (acc == 0).all() and tok[0] == vocab - 3
+    check_accept(p.cpu().numpy(), q.cpu().numpy(), x.cpu().numpy(), u.cpu().numpy(), q_indptr,
+                 acc, tok)
