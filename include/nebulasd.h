@@ -280,7 +280,9 @@ nsd_status nsd_copy_plan_windowed(const void* src, int64_t src_bytes, void* dst,
  * arriving: uint8 [bs]; seq_lens: int32 [bs]; copies: int64 [capacity][3].
  * *n_copies gets the plan's length; if it exceeds capacity only the first
  * capacity triples are written and NSD_ERR_WORKSPACE is returned.  A request
- * with more blocks than the table holds returns NSD_ERR_SHAPE.  Host memory.
+ * with more blocks than the table holds, a negative extent or staging id of an
+ * arriving request, or a byte offset beyond 2^63 - 1 returns NSD_ERR_SHAPE.
+ * Host memory.
  */
 nsd_status nsd_h2d_plan(const int64_t* extent, const int32_t* stage_table,
                         int32_t max_blocks_per_seq, const uint8_t* arriving,
@@ -299,8 +301,9 @@ nsd_status nsd_h2d_plan(const int64_t* extent, const int32_t* stage_table,
  * updated suffix before it is released).
  * block_table: int32 [bs][max_blocks_per_seq]; extent: int64 [bs]; host_len,
  * new_len: int32 [bs]; src_ids, dst_ids: int32 [capacity].  *n_pairs and
- * NSD_ERR_WORKSPACE as nsd_h2d_plan; tokens outside the table or an arena
- * block beyond 2^31 - 1 return an error.  Host memory.
+ * NSD_ERR_WORKSPACE as nsd_h2d_plan; tokens outside the table or a negative
+ * extent of a request with a suffix return NSD_ERR_SHAPE, an arena block
+ * beyond 2^31 - 1 NSD_ERR_UNSUPPORTED.  Host memory.
  */
 nsd_status nsd_writeback_pairs(const int32_t* block_table, int32_t max_blocks_per_seq,
                                const int64_t* extent, const int32_t* host_len,

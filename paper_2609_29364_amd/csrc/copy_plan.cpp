@@ -181,10 +181,19 @@ extern "C" nsd_status nsd_h2d_plan(const int64_t* extent, const int32_t* stage_t
     if (nb > max_blocks_per_seq)
       return fail(NSD_ERR_SHAPE, "%s: request %d has %lld blocks, more than the table's %d", fn,
                   r, (long long)nb, max_blocks_per_seq);
+    // every byte offset of the request must be a non-negative int64
+    const int64_t max_block = INT64_MAX / block_bytes - 1;
+    if (nb > 0 && (extent[r] < 0 || extent[r] > max_block - nb + 1))
+      return fail(NSD_ERR_SHAPE, "%s: request %d: arena extent %lld outside [0, %lld]", fn, r,
+                  (long long)extent[r], (long long)(max_block - nb + 1));
     for (int64_t j = 0; j < nb; ++j, ++n) {
+      const int32_t sid = stage_table[(int64_t)r * max_blocks_per_seq + j];
+      if (sid < 0 || sid > max_block)
+        return fail(NSD_ERR_SHAPE, "%s: request %d block %lld: staging id %d outside [0, %lld]",
+                    fn, r, (long long)j, sid, (long long)max_block);
       if (n >= capacity || !copies) continue;   // counted, not written
       copies[3 * n] = (extent[r] + j) * block_bytes;
-      copies[3 * n + 1] = (int64_t)stage_table[(int64_t)r * max_blocks_per_seq + j] * block_bytes;
+      copies[3 * n + 1] = (int64_t)sid * block_bytes;
       copies[3 * n + 2] = block_bytes;
     }
   }
@@ -217,9 +226,15 @@ extern "C" nsd_status nsd_writeback_pairs(const int32_t* block_table, int32_t ma
     if (h < 0 || (l - 1) / NSD_BLOCK_SIZE >= max_blocks_per_seq)
       return fail(NSD_ERR_SHAPE, "%s: request %d: tokens [%lld, %lld) outside its block table", fn,
                   r, (long long)h, (long long)l);
+    if (extent[r] < 0)
+      return fail(NSD_ERR_SHAPE, "%s: request %d: negative arena extent %lld", fn, r,
+                  (long long)extent[r]);
+    if (extent[r] > INT32_MAX)
+      return fail(NSD_ERR_UNSUPPORTED, "%s: arena block %lld beyond 2^31 - 1", fn,
+                  (long long)extent[r]);
     for (int64_t j = h / NSD_BLOCK_SIZE; j <= (l - 1) / NSD_BLOCK_SIZE; ++j, ++n) {
       if (n >= capacity || !src_ids || !dst_ids) continue;
-      const int64_t a = extent[r] + j;
+      const int64_t a = extent[r] + j;   // both below 2^31: no overflow
       if (a > INT32_MAX)
         return fail(NSD_ERR_UNSUPPORTED, "%s: arena block %lld beyond 2^31 - 1", fn, (long long)a);
       src_ids[n] = block_table[(int64_t)r * max_blocks_per_seq + j];

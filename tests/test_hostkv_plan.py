@@ -79,3 +79,31 @@ def test_writeback_pairs_match_the_oracle():
     s1, d1 = writeback_pairs(bt, extent, host, new)
     s2, d2 = oracle.commit.writeback_pairs(bt, extent, host, new)
     assert np.array_equal(s1, s2) and np.array_equal(d1, d2)
+
+
+def test_plans_refuse_offsets_they_cannot_represent():
+    # negative extents or staging ids and byte offsets past 2^63 - 1 are
+    # refused instead of wrapping around
+    import pytest
+    import paper_2609_29364_amd as nsd
+    from paper_2609_29364_amd.hostkv import writeback_pairs
+    st = np.array([[3, 4]], np.int32)
+    lens = np.array([20], np.int32)
+    arriving = np.array([1], np.uint8)
+    ok = h2d_plan(np.array([5], np.int64), st, arriving, lens, 4096)
+    assert ok.tolist() == [[5 * 4096, 3 * 4096, 4096], [6 * 4096, 4 * 4096, 4096]]
+    for extent, table, block_bytes in (([-1], st, 4096), ([5], np.array([[3, -2]], np.int32), 4096),
+                                       ([2**31 - 1], st, 2**40), ([0], st, 2**62),
+                                       ([2**62], st, 2)):
+        with pytest.raises(nsd.NsdError):
+            h2d_plan(np.array(extent, np.int64), table, arriving, lens, block_bytes)
+    # the largest representable offsets still plan
+    big = h2d_plan(np.array([2**31], np.int64), st, arriving, lens, 2**31)
+    assert big[1].tolist() == [(2**31 + 1) * 2**31, 4 * 2**31, 2**31]
+    bt = np.array([[7, 8]], np.int32)
+    assert [x.tolist() for x in writeback_pairs(bt, np.array([10], np.int64), np.array([0]),
+                                                np.array([20]))] == [[7, 8], [10, 11]]
+    with pytest.raises(nsd.NsdError):
+        writeback_pairs(bt, np.array([-3], np.int64), np.array([0]), np.array([20]))
+    with pytest.raises(nsd.NsdError):
+        writeback_pairs(bt, np.array([2**31], np.int64), np.array([0]), np.array([20]))
