@@ -156,7 +156,8 @@ extern "C" nsd_status nsd_commit_lengths(const int32_t* seq_lens, const int32_t*
   if (!seq_lens || !q_indptr || !accepted_len || !new_lens)
     return fail(NSD_ERR_NULL, "%s: NULL pointer argument", fn);
   clear_stale_error();
-  hipLaunchKernelGGL(commit_kernel, dim3((bs + 255) / 256), dim3(256), 0, (hipStream_t)stream,
+  hipLaunchKernelGGL(commit_kernel, dim3((uint32_t)(((int64_t)bs + 255) / 256)), dim3(256), 0,
+                     (hipStream_t)stream,
                      seq_lens, q_indptr, accepted_len, new_lens, bs);
   return check_launch(fn);
 }

@@ -58,8 +58,8 @@ extern "C" nsd_status nsd_kv_gather(const void* src_k, const void* src_v, int64_
   using namespace nsd;
   if (n_pairs < 0) return fail(NSD_ERR_SHAPE, "kv_gather: n_pairs < 0");
   if (num_layers < 1 || layer0 < 0 || n_layers < 0 || (int64_t)layer0 + n_layers > num_layers)
-    return fail(NSD_ERR_SHAPE, "kv_gather: layer range [%d, %d) outside [0, %d)", layer0,
-                layer0 + n_layers, num_layers);
+    return fail(NSD_ERR_SHAPE, "kv_gather: layer range [%d, %lld) outside [0, %d)", layer0,
+                (long long)layer0 + n_layers, num_layers);
   if (block_size != NSD_BLOCK_SIZE)
     return fail(NSD_ERR_UNSUPPORTED, "kv_gather: block_size must be 16 (got %d)", block_size);
   if (head_dim != 64 && head_dim != 128)

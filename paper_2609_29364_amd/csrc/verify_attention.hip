@@ -1405,7 +1405,7 @@ bool make_plan(int bs, int hq, int hkv, int d, int max_q, int max_seq_len, bool 
   if (bs < 0 || bs > kMaxBatch || hq < 1 || hkv < 1 || hq % hkv || (d != 64 && d != 128) ||
       max_q < 1 || max_seq_len < 0)
     return false;
-  const int rows = (hq / hkv) * max_q;
+  const int64_t rows = (int64_t)(hq / hkv) * max_q;
   if (rows > kMaxRows) return false;
   pl->mt = (rows + 15) / 16;
   pl->lds_bytes = ((size_t)bs + 1) * sizeof(uint32_t) + ((size_t)bs * sizeof(uint16_t) + 3) / 4 * 4;
@@ -1460,9 +1460,9 @@ nsd_status run(const char* fn, bool fuse, const void* q, const void* k_cache,
     return fail(NSD_ERR_SHAPE, "%s: num_q_heads (%d) must be a positive multiple of "
                 "num_kv_heads (%d)", fn, num_q_heads, num_kv_heads);
   if (max_q_per_seq < 1) return fail(NSD_ERR_SHAPE, "%s: max_q_per_seq < 1", fn);
-  if ((num_q_heads / num_kv_heads) * max_q_per_seq > kMaxRows)
-    return fail(NSD_ERR_UNSUPPORTED, "%s: (Hq/Hkv)*max_q_per_seq = %d exceeds %d", fn,
-                (num_q_heads / num_kv_heads) * max_q_per_seq, kMaxRows);
+  if ((int64_t)(num_q_heads / num_kv_heads) * max_q_per_seq > kMaxRows)
+    return fail(NSD_ERR_UNSUPPORTED, "%s: (Hq/Hkv)*max_q_per_seq = %lld exceeds %d", fn,
+                (long long)(num_q_heads / num_kv_heads) * max_q_per_seq, kMaxRows);
   if (max_seq_len < 1 || max_blocks_per_seq < 1 || num_blocks < 1)
     return fail(NSD_ERR_SHAPE, "%s: max_seq_len, max_blocks_per_seq and num_blocks must be "
                 ">= 1", fn);

@@ -73,6 +73,17 @@ def test_attention_validation(lib):
     assert size(4, 5, 2, 64, 5, 256) == 0            # invalid sizes -> 0
     big = size(256, 32, 8, 128, 5, 4096)
     assert big > 0 and big % 16 == 0
+    # a row count past 2^31 is refused, not wrapped
+    assert f(*args(hq=2**30, hkv=1, mq=2**30)) == 3
+    assert size(4, 2**30, 1, 64, 2**30, 256) == 0
+    assert size(4, 2**31 - 1, 1, 64, 128, 256) == 0
+
+
+def test_layer_range_overflow_is_refused(lib):
+    # layer0 + n_layers past 2^31 - 1 is a shape error, found without wrapping
+    st = lib.nsd_kv_gather(None, None, 4, None, None, 4, None, None, 3, 8, 7, 2**31 - 1, 2, 16,
+                           64, None)
+    assert st == 2 and b"layer range" in lib.nsd_last_error()
 
 
 def test_attention_workspace_check(lib):
