@@ -7,8 +7,8 @@
 // bonus row p_K) is 151936 floats in the workloads: streaming it is the whole
 // cost.  A batch with a row for every CU runs accept_row_kernel: one
 // 256-thread workgroup per row takes the acceptance tests, streams the row
-// into chunk sums held in LDS, and draws with one wave, in one launch.  A smaller batch
-// spreads each row over several workgroups, in two kernels:
+// into chunk sums held in LDS, and draws with one wave, in one launch.  A
+// smaller batch spreads each row over several workgroups, in two kernels:
 //
 // 1. row_sums_kernel, one 256-thread workgroup per (row, segment of 64
 //    chunks).  Every workgroup first evaluates the request's K acceptance
@@ -23,8 +23,9 @@
 //    sums into LDS; one wave scans them (a lane owns consecutive chunks; a
 //    wave scan of the lane totals), finds the first chunk whose inclusive
 //    prefix exceeds tau = u_K * S, re-reads that one chunk and picks the
-//    first token t with w(t) > 0 whose running prefix exceeds tau.  A residual without mass (only
-//    possible through fp32 rounding) falls back to p_n, streamed here.
+//    first token t with w(t) > 0 whose running prefix exceeds tau.  A
+//    residual without mass (only possible through fp32 rounding) falls back
+//    to p_n, streamed here.
 // Traffic: each needed row once, plus the chunk sums (8 bytes per 1 KiB) and
 // one 1 KiB chunk per row.
 #include "nsd_internal.h"
@@ -175,12 +176,12 @@ __device__ inline const float* row_p(const Args& A, int r, int a, int n) {
   return SAMPLE ? A.p + (int64_t)r * A.row_stride : A.p + (int64_t)(a + n) * A.vocab;
 }
 
-// One iteration's loads: chunks c0 + u * NW (u < kUnroll) of the weight row, one
-// 16-byte load per lane and chunk (and the draft row's with RESID).  Without
-// CHECK every chunk must be whole and inside [., c_end); with it, chunks past
-// c_end load chunk c_end - 1 again and lanes past the vocabulary its last four
-// weights, so every load is unconditional and in bounds (the reduction drops
-// both).
+// One iteration's loads: chunks c0 + u * NW (u < kUnroll) of the weight
+// row, one 16-byte load per lane and chunk (and the draft row's with RESID).
+// Without CHECK every chunk must be whole and inside [., c_end); with it,
+// chunks past c_end load chunk c_end - 1 again and lanes past the vocabulary
+// its last four weights, so every load is unconditional and in bounds (the
+// reduction drops both).
 template <bool RESID, bool CHECK, int NW>
 __device__ __attribute__((always_inline)) inline void load_chunks(const float* prow, const float* qrow, int vocab, int c0,
                                    int c_end, int lane, f32x4 (&pv)[kUnroll],
