@@ -1,8 +1,9 @@
 """The one-launch acceptance and sampling kernel (a workgroup per row, used
 once a batch has a row for every CU) at the vocabulary sizes where its
 one-wave draw gives each lane the longest run of chunk sums (2^19 weights:
-32 chunks per lane), and the empty-residual fallback of both acceptance
-paths over many chunks, against the oracle."""
+32 chunks per lane), the empty-residual fallback of both acceptance paths
+over many chunks, and strided sampling at the full vocabulary on both
+sampling paths, against the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -75,3 +76,21 @@ def test_empty_residual_draws_from_the_target_row(device, bs):
     assert (acc == 0).all() and tok[0] == vocab - 3
     check_accept(p.cpu().numpy(), q.cpu().numpy(), x.cpu().numpy(), u.cpu().numpy(), q_indptr,
                  acc, tok)
+
+
+@pytest.mark.parametrize("n", [64, ROWS])
+def test_sample_strided_rows_at_full_vocabulary(device, n):
+    # step i of request-major [n][K][V] draft rows (row stride K * V) into
+    # column i of [n][K] tokens (stride K), at the draft vocabulary, on the
+    # two-kernel path (64 rows) and the one-launch kernel (ROWS rows)
+    vocab, k = 151936, 3
+    g = torch.Generator(device=device).manual_seed(n + 3)
+    probs = torch.rand(n, k, vocab, generator=g, device=device) ** 8
+    u = (torch.randint(0, 1 << 24, (k, n), generator=g, device=device) * 2.0**-24).float()
+    tok = torch.full((n, k), -7, dtype=torch.int32, device=device)
+    for i in range(k):
+        nsd.sample(probs[:, i], u[i], out=tok[:, i])
+    torch.cuda.synchronize()
+    tok, u = tok.cpu().numpy(), u.cpu().numpy()
+    for i in range(k):
+        check_samples(probs[:, i].cpu().numpy(), u[i], tok[:, i])
