@@ -5,10 +5,11 @@
 //
 // A request's weight row (max(0, p_n - q_n) after a rejection at n, or the
 // bonus row p_K) is 151936 floats in the workloads: streaming it is the whole
-// cost.  A batch with a row for every CU runs accept_row_kernel: one
-// 256-thread workgroup per row takes the acceptance tests, streams the row
-// into chunk sums held in LDS, and draws with one wave, in one launch.  A
-// smaller batch spreads each row over several workgroups, in two kernels:
+// cost.  A batch with a row for every CU (exactly one, or at least 1.375)
+// runs accept_row_kernel: one 256-thread workgroup per row takes the
+// acceptance tests, streams the row into chunk sums held in LDS, and draws
+// with one wave, in one launch.  Other batches spread each row over several
+// workgroups, in two kernels:
 //
 // 1. row_sums_kernel, one 256-thread workgroup per (row, segment of 64
 //    chunks).  Every workgroup first evaluates the request's K acceptance
@@ -514,10 +515,15 @@ nsd_status launch(bool sample, Args A, int32_t rows, void* workspace, size_t wor
   A.ws_sum = (double*)workspace;
   A.ws_n = (int32_t*)((char*)workspace + sums_bytes(rows, A.vocab));
   const dim3 g1((uint32_t)((A.nchunk + kSegChunks - 1) / kSegChunks) * (uint32_t)rows);
-  // a batch with a row for every CU, or rows of one segment each: one
-  // workgroup per row does both steps (a second launch would add nothing);
-  // otherwise every row is spread over several workgroups
-  const bool one_pass = rows >= device_cus() || A.nchunk <= kSegChunks;
+  // one workgroup per row does both steps (a second launch would add
+  // nothing) for rows of one segment each, or when the batch has a row for
+  // every CU: exactly one, or at least 1.375 (just over one, the few CUs
+  // holding a second row would set the end; below 1.375 rows per CU the
+  // rows spread over all CUs measured faster); otherwise every row is spread
+  // over several workgroups
+  const int cus = device_cus();
+  const bool one_pass =
+      A.nchunk <= kSegChunks || rows == cus || (int64_t)rows * 8 >= (int64_t)cus * 11;
   clear_stale_error();
   if (one_pass) {
     if (sample)

@@ -1,9 +1,9 @@
 """The one-launch acceptance and sampling kernel (a workgroup per row, used
-once a batch has a row for every CU) at the vocabulary sizes where its
-one-wave draw gives each lane the longest run of chunk sums (2^19 weights:
-32 chunks per lane), the empty-residual fallback of both acceptance paths
-over many chunks, and strided sampling at the full vocabulary on both
-sampling paths, against the oracle."""
+when a batch has exactly one row per CU or at least 1.375) at the vocabulary
+sizes where its one-wave draw gives each lane the longest run of chunk sums
+(2^19 weights: 32 chunks per lane), the empty-residual fallback of both
+acceptance paths over many chunks, and strided sampling at the full
+vocabulary on both sampling paths, against the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -14,7 +14,7 @@ from parity import check_accept, check_samples, i32
 
 pytestmark = pytest.mark.gpu
 
-ROWS = 300   # more rows than the MI355X has CUs, so the one-launch kernel runs
+ROWS = 400   # over 1.375 rows per CU of the MI355X (256 CUs): the one-launch kernel
 
 
 @pytest.mark.parametrize("vocab", [1000, 151936, 1 << 19])
@@ -37,8 +37,11 @@ def test_sample_one_launch_matches_oracle(device, vocab):
     check_samples(rows.cpu().numpy(), u.cpu().numpy(), got)
 
 
-def test_accept_one_launch_at_the_largest_vocabulary(device):
-    cfg = custom_config(seed=77, bs=264, num_q_heads=4, num_kv_heads=2, head_dim=64,
+@pytest.mark.parametrize("bs", [300, 360])
+def test_accept_at_the_largest_vocabulary(device, bs):
+    # 300 requests (just over one per CU) take the two-kernel path, 360 the
+    # one-launch kernel
+    cfg = custom_config(seed=77, bs=bs, num_q_heads=4, num_kv_heads=2, head_dim=64,
                         ctx_lo=16, ctx_hi=64, k_lo=0, k_hi=3, n_arriving=0, pool_blocks=None,
                         vocab=1 << 19)
     meta = make_meta(cfg)
