@@ -11,14 +11,14 @@
 // with one wave, in one launch.  Other batches spread each row over several
 // workgroups, in two kernels:
 //
-// 1. row_sums_kernel, one 256-thread workgroup per (row, segment of 64
+// 1. row_sums_kernel, one 256-thread workgroup per (row, segment of 32
 //    chunks).  Every workgroup first evaluates the request's K acceptance
 //    tests u_i * q_i(x_i) <= p_i(x_i) exactly in fp64 (one proposal per lane;
 //    a ballot gives the first rejection n; redundant across a request's
-//    segments, a few scattered loads), then streams its segment of the weight row in 256-element chunks
-//    (one 16-byte load per lane, four chunks of loads in flight per wave,
-//    reduced together in one butterfly) and writes each chunk's fp64 sum to
-//    the workspace.  The row is spread over
+//    segments, a few scattered loads), then streams its segment of the
+//    weight row in 256-element chunks (one 16-byte load per lane, four chunks
+//    of loads in flight per wave, reduced together in one butterfly) and
+//    writes each chunk's fp64 sum to the workspace.  The row is spread over
 //    the whole chip instead of one workgroup per request.
 // 2. pick_kernel, one 256-thread workgroup per row: loads the row's chunk
 //    sums into LDS; one wave scans them (a lane owns consecutive chunks; a
@@ -43,7 +43,8 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kChunk = 256;       // weights per chunk: 64 lanes x 4
 constexpr int kUnroll = 4;
 constexpr int kRowThreads = 256;   // accept_row_kernel: 4 waves per row
-constexpr int kSegChunks = kWaves * kUnroll * 4;   // chunks per row_sums workgroup
+constexpr int kSegChunks = kWaves * kUnroll * 2;   // chunks per row_sums workgroup
+constexpr int kOnePassChunks = 64;   // rows this short always take one workgroup each
 constexpr int kMaxVocab = 1 << 19;
 constexpr int kMaxChunks = kMaxVocab / kChunk;
 constexpr int kMaxK = 63;
@@ -516,14 +517,14 @@ nsd_status launch(bool sample, Args A, int32_t rows, void* workspace, size_t wor
   A.ws_n = (int32_t*)((char*)workspace + sums_bytes(rows, A.vocab));
   const dim3 g1((uint32_t)((A.nchunk + kSegChunks - 1) / kSegChunks) * (uint32_t)rows);
   // one workgroup per row does both steps (a second launch would add
-  // nothing) for rows of one segment each, or when the batch has a row for
+  // nothing) for rows of at most 64 chunks, or when the batch has a row for
   // every CU: exactly one, or at least 1.375 (just over one, the few CUs
   // holding a second row would set the end; below 1.375 rows per CU the
   // rows spread over all CUs measured faster); otherwise every row is spread
   // over several workgroups
   const int cus = device_cus();
   const bool one_pass =
-      A.nchunk <= kSegChunks || rows == cus || (int64_t)rows * 8 >= (int64_t)cus * 11;
+      A.nchunk <= kOnePassChunks || rows == cus || (int64_t)rows * 8 >= (int64_t)cus * 11;
   clear_stale_error();
   if (one_pass) {
     if (sample)
