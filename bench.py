@@ -1257,7 +1257,8 @@ def main():
         # an equivalent rate, not an HBM rate: the bytes the separate gather and
         # attention kernels would move, over the time this path took for that work
         "gather_attention_equiv_tbs": round((alg["gather"] + alg["attention"]) /
-                                            ((g_ms + a_ms) * 1e-3) / 1e12, 3),
+                                            (((g_ms if args.unfused else 0.0) + a_ms) * 1e-3) /
+                                            1e12, 3),
         "roofline": {"bound": "hbm", "kernel": kern, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
