@@ -34,7 +34,7 @@ def _case(seed):
     kind = rng.choice(["none", "all", "some"], p=[0.15, 0.15, 0.7])
     arriving = {"none": np.zeros(bs, bool), "all": np.ones(bs, bool),
                 "some": rng.random(bs) < 0.4}[kind]
-    vocab = int(rng.choice([0, 64, 1000, 4096]))
+    vocab = int(rng.choice([0, 64, 1000, 4096, 16388]))   # 16388: 65 chunks, the two-kernel path
     cfg = custom_config(seed=2000 + seed, bs=bs, num_q_heads=group * hkv, num_kv_heads=hkv,
                         head_dim=d, vocab=vocab, n_arriving=int(arriving.sum()),
                         pool_blocks=None, k_lo=0, k_hi=max_q - 1,
